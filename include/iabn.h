@@ -1,0 +1,173 @@
+/*
+ * libiabn: In-Place Activated Batch Normalization (InPlace-ABN) on AMD
+ * Instinct MI355X (gfx950).
+ *
+ * The method: Rota Bulo, Porzi, Kontschieder, "In-Place Activated BatchNorm
+ * for Memory-Optimized Training of DNNs", CVPR 2018 (arXiv:1712.02616).
+ * A training-mode batch normalisation fused with a leaky ReLU that keeps only
+ * its output z for the backward pass: the forward overwrites x with z
+ * (Algorithm 1), and the backward recovers y = f^-1(z) and
+ * xhat = (y - beta)/gamma from z, then forms the BN gradient (Algorithm 2,
+ * InPlace-ABN I, with the BN backward of Sec. 3.3).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Tensors are NCHW and contiguous, passed as one device pointer plus
+ *    N, C and HW = H*W.  A BN unit is a channel: channel c owns the
+ *    m = N*HW values x[n, c, :] (Sec. 3.1; parameters are channel-specific).
+ *  - Storage type of the activation/gradient tensors: iabn_dtype_t.  All
+ *    per-channel vectors (gamma, beta, running and saved statistics, dgamma,
+ *    dbeta) are fp32 device arrays of length C.  Arithmetic is fp32.
+ *  - The caller owns all memory.  The library never allocates, frees or
+ *    synchronises; every call only enqueues kernels on `stream` (a
+ *    hipStream_t; NULL is the default stream) and returns.  Results are valid
+ *    once the stream has reached them.
+ *  - `workspace` is caller-owned device memory of at least
+ *    iabn_workspace_size(N, C, HW, dtype) bytes, 8-byte aligned.  A forward
+ *    (or backward) split into its two phases must hand the same workspace,
+ *    untouched, from the first phase to the second on the same stream.
+ *  - Errors: every entry point validates its arguments on the host before it
+ *    enqueues anything; on error it returns a nonzero iabn_status_t, changes
+ *    no memory, and iabn_last_error() (per host thread) describes the cause.
+ *    A failed kernel launch returns IABN_ERR_HIP.
+ *  - Not checked, preconditions of the method: gamma[c] != 0 (the inversion
+ *    of the scale-and-shift divides by gamma, Sec. 3.3 "Inversion of pi");
+ *    gamma < 0 is allowed.  Buffers must not overlap except the documented
+ *    in-place pairs.
+ *  - Results are deterministic: the same inputs on the same device give
+ *    bit-identical outputs (all reductions combine in a fixed order).
+ */
+#ifndef IABN_H
+#define IABN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Storage type of x / z / dz / dx. */
+typedef enum {
+    IABN_F32 = 0,  /* IEEE binary32 */
+    IABN_F16 = 1,  /* IEEE binary16; stores round to nearest even */
+    IABN_BF16 = 2  /* bfloat16; stores round to nearest even */
+} iabn_dtype_t;
+
+typedef enum {
+    IABN_OK = 0,
+    IABN_ERR_NULL = 1,      /* a required pointer is NULL */
+    IABN_ERR_SHAPE = 2,     /* N, C or HW out of range, or N*HW < 2 in training */
+    IABN_ERR_PARAM = 3,     /* eps, momentum or slope out of range */
+    IABN_ERR_DTYPE = 4,     /* unknown iabn_dtype_t */
+    IABN_ERR_WORKSPACE = 5, /* workspace too small or misaligned */
+    IABN_ERR_HIP = 6        /* the HIP runtime rejected a launch */
+} iabn_status_t;
+
+/* Library version, major*10000 + minor*100 + patch. */
+int iabn_version(void);
+
+/* Static text for a status code. */
+const char *iabn_status_string(int status);
+
+/* Text describing the last error returned on the calling host thread. */
+const char *iabn_last_error(void);
+
+/* Bytes of workspace the training forward and the backward need for this
+ * shape and storage type (the same amount for both).  Returns 0 for an
+ * invalid shape or dtype. */
+size_t iabn_workspace_size(int64_t N, int64_t C, int64_t HW, int dtype);
+
+/*
+ * Training-mode forward, Algorithm 1, in place.
+ *   x_z            in: x; out: z = f(gamma * (x - mu)/sqrt(sigma^2 + eps) + beta),
+ *                  with the leaky ReLU f(y) = y (y >= 0), slope*y (y < 0) of Sec. 3.3
+ *                  and the per-channel batch mean mu and biased variance
+ *                  sigma^2 of Sec. 3.1 (Eq. 1).
+ *   gamma, beta    [C] scale and shift.
+ *   running_mean, running_var
+ *                  [C], updated in place:
+ *                  running_mean = (1-momentum)*running_mean + momentum*mu,
+ *                  running_var  = (1-momentum)*running_var + momentum*sigma^2*m/(m-1)
+ *                  (the running average of minibatch statistics of Sec. 3.1,
+ *                  with the unbiased variance estimate).
+ *   save_mean, save_var
+ *                  [C] out: mu and the biased sigma^2 (the small buffers that
+ *                  Algorithm 1 keeps for the backward; only sigma^2 is needed
+ *                  there).
+ *   eps > 0, 0 <= momentum <= 1, slope > 0 (f must be invertible, Sec. 3.2/3.3).
+ *   Requires N*HW >= 2.
+ */
+int iabn_forward_train(void *x_z, int dtype, const float *gamma, const float *beta,
+                       float *running_mean, float *running_var, float *save_mean,
+                       float *save_var, float eps, float momentum, float slope, int64_t N,
+                       int64_t C, int64_t HW, void *workspace, size_t workspace_bytes,
+                       void *stream);
+
+/*
+ * Inference-mode forward (Sec. 3.1, statistics fixed to the running
+ * estimates), in place: z = f(gamma * (x - running_mean)/sqrt(running_var + eps) + beta).
+ * Needs no workspace.  eps > 0, slope > 0.
+ */
+int iabn_forward_eval(void *x_z, int dtype, const float *gamma, const float *beta,
+                      const float *running_mean, const float *running_var, float eps,
+                      float slope, int64_t N, int64_t C, int64_t HW, void *stream);
+
+/*
+ * Backward, Algorithm 2 with InPlace-ABN I, in place over the gradient.
+ *   z              [N,C,HW] the forward's output (read only).
+ *   dz_dx          in: dL/dz; out: dL/dx.
+ *   gamma, beta    [C] the forward's parameters.
+ *   save_var       [C] the biased batch variance the forward saved.
+ *   dgamma, dbeta  [C] out (overwritten, not accumulated):
+ *                  dbeta = sum_i dy_i, dgamma = sum_i dy_i * xhat_i, where
+ *                  dy = dz * f'(y), y = f^-1(z), xhat = (y - beta)/gamma.
+ *   dx_i = (dy_i - dgamma*xhat_i/m - dbeta/m) * gamma/sqrt(sigma^2 + eps)  (Sec. 3.3).
+ *   The derivative of f is taken from the stored z: 1 where z >= 0
+ *   (including -0), slope where z < 0.
+ *   eps and slope must be the forward's.  Requires N*HW >= 2.
+ */
+int iabn_backward(const void *z, void *dz_dx, int dtype, const float *gamma, const float *beta,
+                  const float *save_var, float *dgamma, float *dbeta, float eps, float slope,
+                  int64_t N, int64_t C, int64_t HW, void *workspace, size_t workspace_bytes,
+                  void *stream);
+
+/*
+ * The two phases of iabn_forward_train, for callers that need to act between
+ * them (timing each kernel, or combining statistics across devices).
+ * iabn_forward_stats reads x and leaves per-channel partial statistics in the
+ * workspace (Sec. 3.1 mean and variance, not yet combined);
+ * iabn_forward_apply combines them in a fixed order, writes the statistics
+ * and overwrites x with z exactly as iabn_forward_train does.  Arguments mean
+ * what they mean there.
+ */
+int iabn_forward_stats(const void *x, int dtype, int64_t N, int64_t C, int64_t HW,
+                       void *workspace, size_t workspace_bytes, void *stream);
+
+int iabn_forward_apply(void *x_z, int dtype, const float *gamma, const float *beta,
+                       float *running_mean, float *running_var, float *save_mean,
+                       float *save_var, float eps, float momentum, float slope, int64_t N,
+                       int64_t C, int64_t HW, void *workspace, size_t workspace_bytes,
+                       void *stream);
+
+/*
+ * The two phases of iabn_backward.  iabn_backward_reduce reads z and dL/dz
+ * and leaves per-channel partial sums of dy and dy*xhat (Sec. 3.3) in the
+ * workspace; iabn_backward_apply combines them in a fixed order, writes
+ * dgamma and dbeta and overwrites dz_dx with dL/dx exactly as iabn_backward
+ * does.
+ */
+int iabn_backward_reduce(const void *z, const void *dz, int dtype, const float *gamma,
+                         const float *beta, float slope, int64_t N, int64_t C, int64_t HW,
+                         void *workspace, size_t workspace_bytes, void *stream);
+
+int iabn_backward_apply(const void *z, void *dz_dx, int dtype, const float *gamma,
+                        const float *beta, const float *save_var, float *dgamma, float *dbeta,
+                        float eps, float slope, int64_t N, int64_t C, int64_t HW,
+                        void *workspace, size_t workspace_bytes, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* IABN_H */

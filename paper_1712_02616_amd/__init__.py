@@ -1,0 +1,247 @@
+"""Python binding of libiabn: InPlace-ABN (arXiv:1712.02616) on MI355X.
+
+Argument marshalling only.  Every function here has the name and the meaning
+of the C entry point declared in ``include/iabn.h``: it checks that the torch
+tensors have the layout the library expects, passes raw device pointers, the
+shape and the current HIP stream, and turns a nonzero status into
+``IabnError``.  All arithmetic happens in the HIP kernels of ``libiabn.so``;
+there is no other code path, and calls fail if the library cannot be loaded.
+
+Tensors: activations/gradients are contiguous NCHW (any number of trailing
+spatial dims, flattened to HW) in float32, float16 or bfloat16 on a HIP
+device; per-channel tensors are contiguous float32 of length C on the same
+device.  Calls are asynchronous on ``stream`` (default: torch's current
+stream for the tensor's device).
+"""
+
+from __future__ import annotations
+
+import ctypes
+import math
+
+import torch
+
+from . import build as _build
+
+__all__ = [
+    "IabnError", "load", "library_path", "iabn_version", "iabn_status_string",
+    "iabn_workspace_size", "iabn_forward_train", "iabn_forward_eval", "iabn_backward",
+    "iabn_forward_stats", "iabn_forward_apply", "iabn_backward_reduce", "iabn_backward_apply",
+    "DTYPE_CODES",
+]
+
+DTYPE_CODES = {torch.float32: 0, torch.float16: 1, torch.bfloat16: 2}
+
+_lib = None
+
+
+class IabnError(RuntimeError):
+    """A libiabn entry point returned a nonzero status."""
+
+    def __init__(self, fn: str, status: int, detail: str):
+        self.status = status
+        super().__init__("%s failed with status %d: %s" % (fn, status, detail))
+
+
+def library_path() -> str:
+    return _build.LIB
+
+
+def load():
+    """Load libiabn.so (building it first if it has never been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not _build.is_built():
+        _build.build()
+    lib = ctypes.CDLL(_build.LIB)
+    vp, i64, f32, sz, i32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_float, ctypes.c_size_t, ctypes.c_int
+    sig = {
+        "iabn_version": ([], i32),
+        "iabn_status_string": ([i32], ctypes.c_char_p),
+        "iabn_last_error": ([], ctypes.c_char_p),
+        "iabn_workspace_size": ([i64, i64, i64, i32], sz),
+        "iabn_forward_train": ([vp, i32, vp, vp, vp, vp, vp, vp, f32, f32, f32, i64, i64, i64, vp, sz, vp], i32),
+        "iabn_forward_eval": ([vp, i32, vp, vp, vp, vp, f32, f32, i64, i64, i64, vp], i32),
+        "iabn_backward": ([vp, vp, i32, vp, vp, vp, vp, vp, f32, f32, i64, i64, i64, vp, sz, vp], i32),
+        "iabn_forward_stats": ([vp, i32, i64, i64, i64, vp, sz, vp], i32),
+        "iabn_forward_apply": ([vp, i32, vp, vp, vp, vp, vp, vp, f32, f32, f32, i64, i64, i64, vp, sz, vp], i32),
+        "iabn_backward_reduce": ([vp, vp, i32, vp, vp, f32, i64, i64, i64, vp, sz, vp], i32),
+        "iabn_backward_apply": ([vp, vp, i32, vp, vp, vp, vp, vp, f32, f32, i64, i64, i64, vp, sz, vp], i32),
+    }
+    for name, (args, res) in sig.items():
+        fn = getattr(lib, name)
+        fn.argtypes = args
+        fn.restype = res
+    _lib = lib
+    return lib
+
+
+def _check(name: str, rc: int) -> None:
+    if rc != 0:
+        lib = load()
+        raise IabnError(name, rc, (lib.iabn_last_error() or b"").decode() or
+                        lib.iabn_status_string(rc).decode())
+
+
+def _nchw(t: torch.Tensor, what: str):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError("%s must be a torch.Tensor" % what)
+    if t.dim() < 2:
+        raise ValueError("%s must have at least two dims (N, C, ...), got %r" % (what, tuple(t.shape)))
+    if t.dtype not in DTYPE_CODES:
+        raise ValueError("%s has unsupported dtype %s" % (what, t.dtype))
+    if not t.is_contiguous():
+        raise ValueError("%s must be contiguous NCHW" % what)
+    if t.device.type != "cuda":
+        raise ValueError("%s must be on a HIP device" % what)
+    N, C = t.shape[0], t.shape[1]
+    HW = math.prod(t.shape[2:]) if t.dim() > 2 else 1
+    return N, C, HW
+
+
+def _chan(t, C: int, device, what: str):
+    if not isinstance(t, torch.Tensor) or t.dtype != torch.float32 or not t.is_contiguous():
+        raise ValueError("%s must be a contiguous float32 tensor" % what)
+    if t.numel() != C or t.device != device:
+        raise ValueError("%s must hold C=%d values on %s" % (what, C, device))
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _ptr(t: torch.Tensor):
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(device, stream):
+    if stream is None:
+        stream = torch.cuda.current_stream(device)
+    if isinstance(stream, torch.cuda.Stream):
+        return ctypes.c_void_p(stream.cuda_stream)
+    return ctypes.c_void_p(int(stream))
+
+
+def _workspace(N, C, HW, code, device, workspace):
+    need = iabn_workspace_size(N, C, HW, code)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=device)
+    if workspace.device != device or not workspace.is_contiguous():
+        raise ValueError("workspace must be a contiguous tensor on %s" % device)
+    return workspace, ctypes.c_void_p(workspace.data_ptr()), workspace.numel() * workspace.element_size()
+
+
+def iabn_version() -> int:
+    return int(load().iabn_version())
+
+
+def iabn_status_string(status: int) -> str:
+    return load().iabn_status_string(int(status)).decode()
+
+
+def iabn_workspace_size(N: int, C: int, HW: int, dtype) -> int:
+    """Workspace bytes for a shape; ``dtype`` is a torch dtype or a dtype code."""
+    code = DTYPE_CODES[dtype] if isinstance(dtype, torch.dtype) else int(dtype)
+    return int(load().iabn_workspace_size(int(N), int(C), int(HW), code))
+
+
+def iabn_forward_train(x_z, gamma, beta, running_mean, running_var, save_mean, save_var,
+                       eps=1e-5, momentum=0.1, slope=0.01, workspace=None, stream=None):
+    """Training forward (Algorithm 1), in place over ``x_z``; returns ``x_z``."""
+    N, C, HW = _nchw(x_z, "x_z")
+    code = DTYPE_CODES[x_z.dtype]
+    dev = x_z.device
+    args = [_chan(t, C, dev, n) for t, n in ((gamma, "gamma"), (beta, "beta"),
+            (running_mean, "running_mean"), (running_var, "running_var"),
+            (save_mean, "save_mean"), (save_var, "save_var"))]
+    ws, wp, wb = _workspace(N, C, HW, code, dev, workspace)
+    rc = load().iabn_forward_train(_ptr(x_z), code, *args, float(eps), float(momentum),
+                                   float(slope), N, C, HW, wp, wb, _stream(dev, stream))
+    _check("iabn_forward_train", rc)
+    return x_z
+
+
+def iabn_forward_eval(x_z, gamma, beta, running_mean, running_var, eps=1e-5, slope=0.01,
+                      stream=None):
+    """Inference forward with the running statistics, in place; returns ``x_z``."""
+    N, C, HW = _nchw(x_z, "x_z")
+    code = DTYPE_CODES[x_z.dtype]
+    dev = x_z.device
+    args = [_chan(t, C, dev, n) for t, n in ((gamma, "gamma"), (beta, "beta"),
+            (running_mean, "running_mean"), (running_var, "running_var"))]
+    rc = load().iabn_forward_eval(_ptr(x_z), code, *args, float(eps), float(slope), N, C, HW,
+                                  _stream(dev, stream))
+    _check("iabn_forward_eval", rc)
+    return x_z
+
+
+def iabn_backward(z, dz_dx, gamma, beta, save_var, dgamma, dbeta, eps=1e-5, slope=0.01,
+                  workspace=None, stream=None):
+    """Backward (Algorithm 2, InPlace-ABN I), in place over ``dz_dx``; returns ``dz_dx``."""
+    N, C, HW = _nchw(z, "z")
+    if _nchw(dz_dx, "dz_dx") != (N, C, HW) or dz_dx.dtype != z.dtype or dz_dx.device != z.device:
+        raise ValueError("dz_dx must match z in shape, dtype and device")
+    code = DTYPE_CODES[z.dtype]
+    dev = z.device
+    args = [_chan(t, C, dev, n) for t, n in ((gamma, "gamma"), (beta, "beta"),
+            (save_var, "save_var"), (dgamma, "dgamma"), (dbeta, "dbeta"))]
+    ws, wp, wb = _workspace(N, C, HW, code, dev, workspace)
+    rc = load().iabn_backward(_ptr(z), _ptr(dz_dx), code, *args, float(eps), float(slope), N, C, HW,
+                              wp, wb, _stream(dev, stream))
+    _check("iabn_backward", rc)
+    return dz_dx
+
+
+def iabn_forward_stats(x, workspace, stream=None):
+    """First phase of the training forward: partial statistics into ``workspace``."""
+    N, C, HW = _nchw(x, "x")
+    code = DTYPE_CODES[x.dtype]
+    ws, wp, wb = _workspace(N, C, HW, code, x.device, workspace)
+    rc = load().iabn_forward_stats(_ptr(x), code, N, C, HW, wp, wb, _stream(x.device, stream))
+    _check("iabn_forward_stats", rc)
+
+
+def iabn_forward_apply(x_z, gamma, beta, running_mean, running_var, save_mean, save_var,
+                       eps, momentum, slope, workspace, stream=None):
+    """Second phase of the training forward; returns ``x_z``."""
+    N, C, HW = _nchw(x_z, "x_z")
+    code = DTYPE_CODES[x_z.dtype]
+    dev = x_z.device
+    args = [_chan(t, C, dev, n) for t, n in ((gamma, "gamma"), (beta, "beta"),
+            (running_mean, "running_mean"), (running_var, "running_var"),
+            (save_mean, "save_mean"), (save_var, "save_var"))]
+    ws, wp, wb = _workspace(N, C, HW, code, dev, workspace)
+    rc = load().iabn_forward_apply(_ptr(x_z), code, *args, float(eps), float(momentum),
+                                   float(slope), N, C, HW, wp, wb, _stream(dev, stream))
+    _check("iabn_forward_apply", rc)
+    return x_z
+
+
+def iabn_backward_reduce(z, dz, gamma, beta, slope, workspace, stream=None):
+    """First phase of the backward: partial sums of dy and dy*xhat into ``workspace``."""
+    N, C, HW = _nchw(z, "z")
+    if _nchw(dz, "dz") != (N, C, HW) or dz.dtype != z.dtype or dz.device != z.device:
+        raise ValueError("dz must match z in shape, dtype and device")
+    code = DTYPE_CODES[z.dtype]
+    dev = z.device
+    g = _chan(gamma, C, dev, "gamma")
+    b = _chan(beta, C, dev, "beta")
+    ws, wp, wb = _workspace(N, C, HW, code, dev, workspace)
+    rc = load().iabn_backward_reduce(_ptr(z), _ptr(dz), code, g, b, float(slope), N, C, HW, wp, wb,
+                                     _stream(dev, stream))
+    _check("iabn_backward_reduce", rc)
+
+
+def iabn_backward_apply(z, dz_dx, gamma, beta, save_var, dgamma, dbeta, eps, slope, workspace,
+                        stream=None):
+    """Second phase of the backward; returns ``dz_dx``."""
+    N, C, HW = _nchw(z, "z")
+    if _nchw(dz_dx, "dz_dx") != (N, C, HW) or dz_dx.dtype != z.dtype or dz_dx.device != z.device:
+        raise ValueError("dz_dx must match z in shape, dtype and device")
+    code = DTYPE_CODES[z.dtype]
+    dev = z.device
+    args = [_chan(t, C, dev, n) for t, n in ((gamma, "gamma"), (beta, "beta"),
+            (save_var, "save_var"), (dgamma, "dgamma"), (dbeta, "dbeta"))]
+    ws, wp, wb = _workspace(N, C, HW, code, dev, workspace)
+    rc = load().iabn_backward_apply(_ptr(z), _ptr(dz_dx), code, *args, float(eps), float(slope),
+                                    N, C, HW, wp, wb, _stream(dev, stream))
+    _check("iabn_backward_apply", rc)
+    return dz_dx
