@@ -17,13 +17,14 @@
  *    m = N*HW values x[n, c, :] (Sec. 3.1; parameters are channel-specific).
  *  - Storage type of the activation/gradient tensors: iabn_dtype_t.  All
  *    per-channel vectors (gamma, beta, running and saved statistics, dgamma,
- *    dbeta) are fp32 device arrays of length C.  Arithmetic is fp32.
+ *    dbeta) are fp32 device arrays of length C.  Per-element arithmetic is
+ *    fp32; reductions combine per-thread partial results in fp64.
  *  - The caller owns all memory.  The library never allocates, frees or
  *    synchronises; every call only enqueues kernels on `stream` (a
  *    hipStream_t; NULL is the default stream) and returns.  Results are valid
  *    once the stream has reached them.
  *  - `workspace` is caller-owned device memory of at least
- *    iabn_workspace_size(N, C, HW, dtype) bytes, 8-byte aligned.  A forward
+ *    iabn_workspace_size(N, C, HW, dtype) bytes, 16-byte aligned.  A forward
  *    (or backward) split into its two phases must hand the same workspace,
  *    untouched, from the first phase to the second on the same stream.
  *  - Errors: every entry point validates its arguments on the host before it

@@ -116,7 +116,7 @@ struct Geom {
     uint32_t vec;    // elements per access
     iabn_divmagic_t row_div;  // division by vrow
     uint64_t nstride;         // accesses between samples of a channel (C * vrow)
-    float m;                  // elements per channel (N * HW)
+    double m;                 // elements per channel (N * HW)
 };
 
 // Index (in accesses) of the v-th access of channel c.
@@ -140,36 +140,32 @@ __device__ __forceinline__ Slice block_slice(const Geom& g) {
 }
 
 // Elements in slice p of a channel.
-__device__ __forceinline__ float slice_count(const Geom& g, uint32_t p) {
+__device__ __forceinline__ double slice_count(const Geom& g, uint32_t p) {
     const uint32_t lo = p * g.lv;
     const uint32_t hi = min(lo + g.lv, g.vchan);
-    return static_cast<float>(hi - lo) * static_cast<float>(g.vec);
+    return static_cast<double>(hi - lo) * static_cast<double>(g.vec);
 }
 
 // ---------------------------------------------------------------- reductions
 
-// Count, mean and sum of squared deviations of a set of values.  Two sets
-// combine with the pairwise update of Chan, Golub and LeVeque (1979).
+// Count, mean and sum of squared deviations of a set of values, in double.
+// Two sets combine with the pairwise update of Chan, Golub and LeVeque
+// (1979).  Per-element work stays in fp32 (see fwd_stats_kernel); only the
+// per-thread results and everything after them are double, which costs a few
+// dozen instructions per thread and keeps large channel means from eating
+// the fp32 mantissa.
 struct Moments {
-    float n, mean, m2;
+    double n, mean, m2;
 };
 
 __device__ __forceinline__ Moments chan_merge(const Moments& a, const Moments& b) {
-    const float n = a.n + b.n;
-    const float wb = n > 0.f ? b.n / n : 0.f;
-    const float d = b.mean - a.mean;
+    const double n = a.n + b.n;
+    const double wb = n > 0.0 ? b.n / n : 0.0;
+    const double d = b.mean - a.mean;
     Moments r;
     r.n = n;
-    r.mean = fmaf(d, wb, a.mean);
+    r.mean = fma(d, wb, a.mean);
     r.m2 = a.m2 + b.m2 + d * d * a.n * wb;
-    return r;
-}
-
-__device__ __forceinline__ Moments shfl_down(const Moments& a, int off) {
-    Moments r;
-    r.n = __shfl_down(a.n, off, kWave);
-    r.mean = __shfl_down(a.mean, off, kWave);
-    r.m2 = __shfl_down(a.m2, off, kWave);
     return r;
 }
 
@@ -177,13 +173,16 @@ __device__ __forceinline__ Moments shfl_down(const Moments& a, int off) {
 __device__ __forceinline__ Moments wave_merge(Moments a) {
 #pragma unroll
     for (int off = kWave / 2; off > 0; off >>= 1) {
-        const Moments b = shfl_down(a, off);
+        Moments b;
+        b.n = __shfl_down(a.n, off, kWave);
+        b.mean = __shfl_down(a.mean, off, kWave);
+        b.m2 = __shfl_down(a.m2, off, kWave);
         if ((threadIdx.x & (kWave - 1)) < static_cast<unsigned>(off)) a = chan_merge(a, b);
     }
     return a;
 }
 
-__device__ __forceinline__ float2 wave_sum2(float2 a) {
+__device__ __forceinline__ double2 wave_sum(double2 a) {
 #pragma unroll
     for (int off = kWave / 2; off > 0; off >>= 1) {
         a.x += __shfl_down(a.x, off, kWave);
@@ -192,78 +191,92 @@ __device__ __forceinline__ float2 wave_sum2(float2 a) {
     return a;
 }
 
-// Moments of a block of values, two passes over registers.
-template <int K>
-__device__ __forceinline__ Moments moments_of(const float (&v)[K]) {
-    float s = 0.f;
-#pragma unroll
-    for (int k = 0; k < K; ++k) s += v[k];
-    Moments r;
-    r.n = static_cast<float>(K);
-    r.mean = s * (1.0f / static_cast<float>(K));
-    float q = 0.f;
-#pragma unroll
-    for (int k = 0; k < K; ++k) {
-        const float d = v[k] - r.mean;
-        q = fmaf(d, d, q);
-    }
-    r.m2 = q;
-    return r;
-}
-
 // Combine a channel's P partial moments (fixed order); run by one full wave,
 // the result is valid in lane 0.
 __device__ __forceinline__ Moments combine_channel_moments(const Geom& g,
-                                                           const float2* __restrict__ part,
+                                                           const double2* __restrict__ part,
                                                            uint32_t c) {
     const uint32_t lane = threadIdx.x & (kWave - 1);
-    Moments acc = {0.f, 0.f, 0.f};
+    Moments acc = {0.0, 0.0, 0.0};
     for (uint32_t p = lane; p < g.P; p += kWave) {
-        const float2 pm = part[static_cast<uint64_t>(c) * g.P + p];
+        const double2 pm = part[static_cast<uint64_t>(c) * g.P + p];
         const Moments b = {slice_count(g, p), pm.x, pm.y};
         acc = chan_merge(acc, b);
     }
     return wave_merge(acc);
 }
 
-__device__ __forceinline__ float2 combine_channel_sums(const Geom& g,
-                                                       const float2* __restrict__ part,
-                                                       uint32_t c) {
+__device__ __forceinline__ double2 combine_channel_sums(const Geom& g,
+                                                        const double2* __restrict__ part,
+                                                        uint32_t c) {
     const uint32_t lane = threadIdx.x & (kWave - 1);
-    float2 acc = make_float2(0.f, 0.f);
+    double2 acc = make_double2(0.0, 0.0);
     for (uint32_t p = lane; p < g.P; p += kWave) {
-        const float2 s = part[static_cast<uint64_t>(c) * g.P + p];
+        const double2 s = part[static_cast<uint64_t>(c) * g.P + p];
         acc.x += s.x;
         acc.y += s.y;
     }
-    return wave_sum2(acc);
+    return wave_sum(acc);
 }
 
 // ---------------------------------------------------------------- forward
 
-// Partial moments of one (channel, slice).  part[c*P + p] = (mean, M2).
+// Partial moments of one (channel, slice): part[c*P + p] = (mean, M2).
+//
+// Each thread accumulates shifted sums S1 = sum(x - K), S2 = sum((x - K)^2)
+// in fp32 with K = the first value it reads, which sits within a few standard
+// deviations of the mean, so x - K carries the spread and not the offset
+// (and is exact when x and K are within a factor of two).  The thread's
+// moments are then mean = K + S1/n, M2 = S2 - S1^2/n, formed in double.
 template <int DT, int VEC, int U>
 __global__ __launch_bounds__(kThreads) void fwd_stats_kernel(const void* __restrict__ x, Geom g,
-                                                             float2* __restrict__ part) {
+                                                             double2* __restrict__ part) {
     const Slice s = block_slice(g);
     const uint64_t cbase = static_cast<uint64_t>(s.c) * g.vrow;
-    Moments acc = {0.f, 0.f, 0.f};
+    float shift = 0.f, s1 = 0.f, s2 = 0.f;
+    bool first = true;
+    uint32_t nacc = 0;
     uint32_t v = s.lo + threadIdx.x;
     for (; v + (U - 1) * kThreads < s.hi; v += U * kThreads) {
-        float vals[U * VEC];
+        float t[U][VEC];
+#pragma unroll
+        for (int u = 0; u < U; ++u) load_vec<DT, VEC>(x, access_index(g, cbase, v + u * kThreads), t[u]);
+        if (first) shift = t[0][0];
+        first = false;
+        float a1 = 0.f, a2 = 0.f;
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            float t[VEC];
-            load_vec<DT, VEC>(x, access_index(g, cbase, v + u * kThreads), t);
 #pragma unroll
-            for (int k = 0; k < VEC; ++k) vals[u * VEC + k] = t[k];
+            for (int k = 0; k < VEC; ++k) {
+                const float d = t[u][k] - shift;
+                a1 += d;
+                a2 = fmaf(d, d, a2);
+            }
         }
-        acc = chan_merge(acc, moments_of<U * VEC>(vals));
+        s1 += a1;
+        s2 += a2;
+        nacc += U;
     }
     for (; v < s.hi; v += kThreads) {
         float t[VEC];
         load_vec<DT, VEC>(x, access_index(g, cbase, v), t);
-        acc = chan_merge(acc, moments_of<VEC>(t));
+        if (first) shift = t[0];
+        first = false;
+#pragma unroll
+        for (int k = 0; k < VEC; ++k) {
+            const float d = t[k] - shift;
+            s1 += d;
+            s2 = fmaf(d, d, s2);
+        }
+        nacc += 1;
+    }
+    Moments acc = {0.0, 0.0, 0.0};
+    if (nacc > 0) {
+        const double n = static_cast<double>(nacc) * g.vec;
+        const double d1 = s1, d2 = s2;
+        acc.n = n;
+        acc.mean = static_cast<double>(shift) + d1 / n;
+        acc.m2 = fmax(d2 - d1 * d1 / n, 0.0);
     }
     acc = wave_merge(acc);
 
@@ -275,7 +288,7 @@ __global__ __launch_bounds__(kThreads) void fwd_stats_kernel(const void* __restr
         Moments r = wave_acc[0];
 #pragma unroll
         for (int w = 1; w < kWaves; ++w) r = chan_merge(r, wave_acc[w]);
-        part[static_cast<uint64_t>(s.c) * g.P + s.p] = make_float2(r.mean, fmaxf(r.m2, 0.f));
+        part[static_cast<uint64_t>(s.c) * g.P + s.p] = make_double2(r.mean, r.m2);
     }
 }
 
@@ -292,47 +305,53 @@ struct FwdParams {
 // z = f(gamma * (x - mu) / sqrt(var + eps) + beta), in place.  TRAIN: mu and
 // var are the batch statistics combined from the partials (slice 0 of each
 // channel also writes them out and updates the running estimates); otherwise
-// they are the running estimates.
+// they are the running estimates.  mu is applied as a two-float sum
+// hi + lo, so x - mu keeps fp32 relative accuracy even when |mu| >> sigma.
 template <int DT, int VEC, int U, bool TRAIN>
 __global__ __launch_bounds__(kThreads) void fwd_apply_kernel(void* __restrict__ xz, Geom g,
-                                                             const float2* __restrict__ part,
+                                                             const double2* __restrict__ part,
                                                              FwdParams prm) {
     const Slice s = block_slice(g);
-    __shared__ float coef[3];
+    __shared__ float coef[4];
     if (threadIdx.x < kWave) {
-        float mean, var;
+        double mean, var;
         if constexpr (TRAIN) {
             const Moments r = combine_channel_moments(g, part, s.c);
             mean = r.mean;
-            var = fmaxf(r.m2, 0.f) / g.m;
+            var = fmax(r.m2, 0.0) / g.m;
         } else {
             mean = prm.running_mean[s.c];
             var = prm.running_var[s.c];
         }
         if (threadIdx.x == 0) {
-            const float invstd = 1.0f / sqrtf(var + prm.eps);
-            coef[0] = mean;
-            coef[1] = prm.gamma[s.c] * invstd;
-            coef[2] = prm.beta[s.c];
+            const double scale = static_cast<double>(prm.gamma[s.c]) / sqrt(var + static_cast<double>(prm.eps));
+            const float mean_hi = static_cast<float>(mean);
+            coef[0] = mean_hi;
+            coef[1] = static_cast<float>(mean - static_cast<double>(mean_hi));
+            coef[2] = static_cast<float>(scale);
+            coef[3] = prm.beta[s.c];
             if constexpr (TRAIN) {
                 if (s.p == 0) {
-                    prm.save_mean[s.c] = mean;
-                    prm.save_var[s.c] = var;
-                    const float mom = prm.momentum;
-                    prm.running_mean[s.c] = (1.f - mom) * prm.running_mean[s.c] + mom * mean;
-                    prm.running_var[s.c] =
-                        (1.f - mom) * prm.running_var[s.c] + mom * var * (g.m / (g.m - 1.f));
+                    const double mom = prm.momentum;
+                    const double m = g.m;
+                    prm.save_mean[s.c] = mean_hi;
+                    prm.save_var[s.c] = static_cast<float>(var);
+                    prm.running_mean[s.c] = static_cast<float>(
+                        (1.0 - mom) * static_cast<double>(prm.running_mean[s.c]) + mom * mean);
+                    prm.running_var[s.c] = static_cast<float>(
+                        (1.0 - mom) * static_cast<double>(prm.running_var[s.c]) +
+                        mom * var * (m / (m - 1.0)));
                 }
             }
         }
     }
     __syncthreads();
-    const float mean = coef[0], scale = coef[1], shift = coef[2];
+    const float mean_hi = coef[0], mean_lo = coef[1], scale = coef[2], shift = coef[3];
     const float slope = prm.slope;
     const uint64_t cbase = static_cast<uint64_t>(s.c) * g.vrow;
 
     auto act = [&](float xv) {
-        const float y = fmaf(xv - mean, scale, shift);
+        const float y = fmaf((xv - mean_hi) - mean_lo, scale, shift);
         return y >= 0.f ? y : slope * y;
     };
 
@@ -378,18 +397,20 @@ struct BwdElem {
     }
 };
 
-// Partial sums of dy and dy*xhat of one (channel, slice).  part[c*P+p] = (sum dy, sum dy*xhat).
+// Partial sums of dy and dy*xhat of one (channel, slice):
+// part[c*P + p] = (sum dy, sum dy*xhat).  fp32 per batch of U accesses,
+// double across batches and threads.
 template <int DT, int VEC, int U>
 __global__ __launch_bounds__(kThreads) void bwd_reduce_kernel(const void* __restrict__ z,
                                                               const void* __restrict__ dz, Geom g,
                                                               const float* __restrict__ gamma,
                                                               const float* __restrict__ beta,
                                                               float slope,
-                                                              float2* __restrict__ part) {
+                                                              double2* __restrict__ part) {
     const Slice s = block_slice(g);
     const BwdElem el = {slope, 1.0f / slope, beta[s.c], 1.0f / gamma[s.c]};
     const uint64_t cbase = static_cast<uint64_t>(s.c) * g.vrow;
-    float2 acc = make_float2(0.f, 0.f);
+    double2 acc = make_double2(0.0, 0.0);
     uint32_t v = s.lo + threadIdx.x;
     for (; v + (U - 1) * kThreads < s.hi; v += U * kThreads) {
         float tz[U][VEC], tg[U][VEC];
@@ -429,14 +450,14 @@ __global__ __launch_bounds__(kThreads) void bwd_reduce_kernel(const void* __rest
         acc.x += sdy;
         acc.y += sdyx;
     }
-    acc = wave_sum2(acc);
+    acc = wave_sum(acc);
 
-    __shared__ float2 wave_acc[kWaves];
+    __shared__ double2 wave_acc[kWaves];
     const uint32_t wave = threadIdx.x / kWave;
     if ((threadIdx.x & (kWave - 1)) == 0) wave_acc[wave] = acc;
     __syncthreads();
     if (threadIdx.x == 0) {
-        float2 r = wave_acc[0];
+        double2 r = wave_acc[0];
 #pragma unroll
         for (int w = 1; w < kWaves; ++w) {
             r.x += wave_acc[w].x;
@@ -455,25 +476,27 @@ struct BwdParams {
     float eps, slope;
 };
 
-// dx = (dy - dgamma*xhat/m - dbeta/m) * gamma/sqrt(var + eps), in place over dz.
+// dx = (dy - dgamma*xhat/m - dbeta/m) * gamma/sqrt(var + eps), in place over dz,
+// as dx = A*dy + B*xhat + Cc with per-channel A, B, Cc formed in double.
 template <int DT, int VEC, int U>
 __global__ __launch_bounds__(kThreads) void bwd_apply_kernel(const void* __restrict__ z,
                                                              void* __restrict__ dzdx, Geom g,
-                                                             const float2* __restrict__ part,
+                                                             const double2* __restrict__ part,
                                                              BwdParams prm) {
     const Slice s = block_slice(g);
     __shared__ float coef[3];
     if (threadIdx.x < kWave) {
-        const float2 sums = combine_channel_sums(g, part, s.c);
+        const double2 sums = combine_channel_sums(g, part, s.c);
         if (threadIdx.x == 0) {
-            const float dbeta = sums.x, dgamma = sums.y;
-            const float a = prm.gamma[s.c] / sqrtf(prm.save_var[s.c] + prm.eps);
-            coef[0] = a;
-            coef[1] = -a * dgamma / g.m;
-            coef[2] = -a * dbeta / g.m;
+            const double dbeta = sums.x, dgamma = sums.y, m = g.m;
+            const double a = static_cast<double>(prm.gamma[s.c]) /
+                             sqrt(static_cast<double>(prm.save_var[s.c]) + static_cast<double>(prm.eps));
+            coef[0] = static_cast<float>(a);
+            coef[1] = static_cast<float>(-a * dgamma / m);
+            coef[2] = static_cast<float>(-a * dbeta / m);
             if (s.p == 0) {
-                prm.dgamma[s.c] = dgamma;
-                prm.dbeta[s.c] = dbeta;
+                prm.dgamma[s.c] = static_cast<float>(dgamma);
+                prm.dbeta[s.c] = static_cast<float>(dbeta);
             }
         }
     }
@@ -583,7 +606,7 @@ int check_shape(int64_t N, int64_t C, int64_t HW, bool train) {
 size_t workspace_bytes_for(int64_t N, int64_t C, int64_t HW) {
     if (C == 0 || N * HW == 0) return 0;
     const Split sp = split_channel(N * HW, C);
-    return static_cast<size_t>(C) * static_cast<size_t>(sp.P) * sizeof(float2);
+    return static_cast<size_t>(C) * static_cast<size_t>(sp.P) * sizeof(double2);
 }
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
@@ -603,7 +626,7 @@ Geom make_geom(int64_t N, int64_t C, int64_t HW, int dtype, bool vector) {
     g.vec = static_cast<uint32_t>(vec);
     g.row_div = iabn_divmagic_make(g.vrow);
     g.nstride = static_cast<uint64_t>(C) * g.vrow;
-    g.m = static_cast<float>(m);
+    g.m = static_cast<double>(m);
     return g;
 }
 
@@ -618,8 +641,8 @@ int check_workspace(int64_t N, int64_t C, int64_t HW, const void* ws, size_t byt
     if (ws == nullptr) return fail(IABN_ERR_NULL, "workspace is NULL (%zu bytes needed)", need);
     if (bytes < need)
         return fail(IABN_ERR_WORKSPACE, "workspace has %zu bytes, %zu needed", bytes, need);
-    if ((reinterpret_cast<uintptr_t>(ws) & 7u) != 0)
-        return fail(IABN_ERR_WORKSPACE, "workspace is not 8-byte aligned");
+    if ((reinterpret_cast<uintptr_t>(ws) & 15u) != 0)
+        return fail(IABN_ERR_WORKSPACE, "workspace is not 16-byte aligned");
     return IABN_OK;
 }
 
@@ -666,14 +689,14 @@ constexpr int unroll() {
 
 template <int DT, int VEC>
 struct LaunchFwdStats {
-    static void run(const void* x, const Geom& g, float2* part, hipStream_t st) {
+    static void run(const void* x, const Geom& g, double2* part, hipStream_t st) {
         fwd_stats_kernel<DT, VEC, unroll<VEC>()><<<grid_of(g), kThreads, 0, st>>>(x, g, part);
     }
 };
 
 template <int DT, int VEC>
 struct LaunchFwdApply {
-    static void run(void* xz, const Geom& g, const float2* part, const FwdParams& prm, bool train,
+    static void run(void* xz, const Geom& g, const double2* part, const FwdParams& prm, bool train,
                     hipStream_t st) {
         if (train)
             fwd_apply_kernel<DT, VEC, unroll<VEC>(), true><<<grid_of(g), kThreads, 0, st>>>(
@@ -687,7 +710,7 @@ struct LaunchFwdApply {
 template <int DT, int VEC>
 struct LaunchBwdReduce {
     static void run(const void* z, const void* dz, const Geom& g, const float* gamma,
-                    const float* beta, float slope, float2* part, hipStream_t st) {
+                    const float* beta, float slope, double2* part, hipStream_t st) {
         bwd_reduce_kernel<DT, VEC, unroll<VEC>()><<<grid_of(g), kThreads, 0, st>>>(
             z, dz, g, gamma, beta, slope, part);
     }
@@ -695,7 +718,7 @@ struct LaunchBwdReduce {
 
 template <int DT, int VEC>
 struct LaunchBwdApply {
-    static void run(const void* z, void* dzdx, const Geom& g, const float2* part,
+    static void run(const void* z, void* dzdx, const Geom& g, const double2* part,
                     const BwdParams& prm, hipStream_t st) {
         bwd_apply_kernel<DT, VEC, unroll<VEC>()><<<grid_of(g), kThreads, 0, st>>>(z, dzdx, g,
                                                                                    part, prm);
@@ -747,7 +770,7 @@ int iabn_forward_stats(const void* x, int dtype, int64_t N, int64_t C, int64_t H
     if ((rc = check_workspace(N, C, HW, workspace, workspace_bytes))) return rc;
     const bool vec = use_vector(HW, dtype, x, nullptr);
     const Geom g = make_geom(N, C, HW, dtype, vec);
-    dispatch<LaunchFwdStats>(dtype, vec, x, g, static_cast<float2*>(workspace),
+    dispatch<LaunchFwdStats>(dtype, vec, x, g, static_cast<double2*>(workspace),
                              static_cast<hipStream_t>(stream));
     return launched("fwd_stats");
 }
@@ -770,7 +793,7 @@ int iabn_forward_apply(void* x_z, int dtype, const float* gamma, const float* be
     const Geom g = make_geom(N, C, HW, dtype, vec);
     const FwdParams prm = {gamma, beta, running_mean, running_var, save_mean, save_var,
                            eps,   momentum, slope};
-    dispatch<LaunchFwdApply>(dtype, vec, x_z, g, static_cast<const float2*>(workspace), prm, true,
+    dispatch<LaunchFwdApply>(dtype, vec, x_z, g, static_cast<const double2*>(workspace), prm, true,
                              static_cast<hipStream_t>(stream));
     return launched("fwd_apply");
 }
@@ -810,7 +833,7 @@ int iabn_forward_eval(void* x_z, int dtype, const float* gamma, const float* bet
     const Geom g = make_geom(N, C, HW, dtype, vec);
     const FwdParams prm = {gamma, beta, const_cast<float*>(running_mean),
                            const_cast<float*>(running_var), nullptr, nullptr, eps, 0.f, slope};
-    dispatch<LaunchFwdApply>(dtype, vec, x_z, g, static_cast<const float2*>(nullptr), prm, false,
+    dispatch<LaunchFwdApply>(dtype, vec, x_z, g, static_cast<const double2*>(nullptr), prm, false,
                              static_cast<hipStream_t>(stream));
     return launched("fwd_eval");
 }
@@ -829,7 +852,7 @@ int iabn_backward_reduce(const void* z, const void* dz, int dtype, const float* 
     const bool vec = use_vector(HW, dtype, z, dz);
     const Geom g = make_geom(N, C, HW, dtype, vec);
     dispatch<LaunchBwdReduce>(dtype, vec, z, dz, g, gamma, beta, slope,
-                              static_cast<float2*>(workspace), static_cast<hipStream_t>(stream));
+                              static_cast<double2*>(workspace), static_cast<hipStream_t>(stream));
     return launched("bwd_reduce");
 }
 
@@ -847,7 +870,7 @@ int iabn_backward_apply(const void* z, void* dz_dx, int dtype, const float* gamm
     const bool vec = use_vector(HW, dtype, z, dz_dx);
     const Geom g = make_geom(N, C, HW, dtype, vec);
     const BwdParams prm = {gamma, beta, save_var, dgamma, dbeta, eps, slope};
-    dispatch<LaunchBwdApply>(dtype, vec, z, dz_dx, g, static_cast<const float2*>(workspace), prm,
+    dispatch<LaunchBwdApply>(dtype, vec, z, dz_dx, g, static_cast<const double2*>(workspace), prm,
                              static_cast<hipStream_t>(stream));
     return launched("bwd_apply");
 }

@@ -79,7 +79,7 @@ def _split(m, C):
                                     (8, 1024, 4096), (8, 2048, 4096), (3, 5, 7), (1, 1, 2)])
 def test_workspace_size(lib, N, C, HW):
     for dt in (F32, F16, BF16):
-        assert lib.iabn_workspace_size(N, C, HW, dt) == C * _split(N * HW, C) * 8
+        assert lib.iabn_workspace_size(N, C, HW, dt) == C * _split(N * HW, C) * 16
 
 
 def test_workspace_size_invalid(lib):
@@ -122,6 +122,7 @@ def test_forward_train_validation(lib):
     assert fwd(lib, mom=float("nan")) == ERR_PARAM
     assert fwd(lib, ws=NULL) == ERR_NULL
     assert fwd(lib, wsb=8) == ERR_WORKSPACE
+    assert fwd(lib, ws=ctypes.c_void_p(0x1008)) == ERR_WORKSPACE
     assert fwd(lib, ws=ctypes.c_void_p(0x1004)) == ERR_WORKSPACE
     assert b"workspace" in lib.iabn_last_error()
 
