@@ -28,10 +28,11 @@
 // threads.  The backward's apply kernel reads dz before overwriting it, and
 // runs after the reduce kernel on the same stream.
 //
-// Determinism.  Each block reduces in a fixed shuffle tree, then across its
-// four waves in a fixed order; the apply kernels combine a channel's P
-// partials in a fixed tree.  Nothing depends on scheduling, so results are
-// bit-identical from run to run.
+// Reductions.  Every wave of a reduction kernel writes one partial result
+// (no block barrier); each wave of an apply kernel combines its channel's
+// partials itself, while its first data loads are already in flight.  All
+// combines run in a fixed order, so results are bit-identical from run to
+// run.
 
 #include <hip/hip_runtime.h>
 
@@ -71,17 +72,25 @@ struct Elem<IABN_BF16> {
     using T = __bf16;
 };
 
+// Cache hint of an access: kCached for data that is read again soon (it
+// should stay in the caches), kStream for the last touch of a tensor in a
+// pass (non-temporal: do not displace data that is reused).
+constexpr int kCached = 0;
+constexpr int kStream = 1;
+
 // VEC elements per access: 16 bytes on the vector path, 1 on the scalar path.
-template <int DT, int VEC>
+template <int DT, int VEC, int HINT>
 __device__ __forceinline__ void load_vec(const void* __restrict__ base, uint64_t idx,
                                          float (&v)[VEC]) {
     using T = typename Elem<DT>::T;
     if constexpr (VEC == 1) {
-        v[0] = static_cast<float>(static_cast<const T*>(base)[idx]);
+        const T* p = static_cast<const T*>(base) + idx;
+        v[0] = static_cast<float>(HINT == kStream ? __builtin_nontemporal_load(p) : *p);
     } else {
         typedef T vt __attribute__((ext_vector_type(VEC)));
         typedef float vf __attribute__((ext_vector_type(VEC)));
-        const vt r = static_cast<const vt*>(base)[idx];
+        const vt* p = static_cast<const vt*>(base) + idx;
+        const vt r = HINT == kStream ? __builtin_nontemporal_load(p) : *p;
         const vf f = __builtin_convertvector(r, vf);
 #pragma unroll
         for (int k = 0; k < VEC; ++k) v[k] = f[k];
@@ -89,27 +98,44 @@ __device__ __forceinline__ void load_vec(const void* __restrict__ base, uint64_t
 }
 
 // fp32 -> storage conversions round to nearest even.
-template <int DT, int VEC>
+template <int DT, int VEC, int HINT>
 __device__ __forceinline__ void store_vec(void* __restrict__ base, uint64_t idx,
                                           const float (&v)[VEC]) {
     using T = typename Elem<DT>::T;
     if constexpr (VEC == 1) {
-        static_cast<T*>(base)[idx] = static_cast<T>(v[0]);
+        T* p = static_cast<T*>(base) + idx;
+        const T r = static_cast<T>(v[0]);
+        if constexpr (HINT == kStream) __builtin_nontemporal_store(r, p);
+        else *p = r;
     } else {
         typedef T vt __attribute__((ext_vector_type(VEC)));
         typedef float vf __attribute__((ext_vector_type(VEC)));
         vf f;
 #pragma unroll
         for (int k = 0; k < VEC; ++k) f[k] = v[k];
-        static_cast<vt*>(base)[idx] = __builtin_convertvector(f, vt);
+        const vt r = __builtin_convertvector(f, vt);
+        vt* p = static_cast<vt*>(base) + idx;
+        if constexpr (HINT == kStream) __builtin_nontemporal_store(r, p);
+        else *p = r;
     }
 }
+
+// Cache hints of the four passes.  x is read by the statistics pass and
+// again by the forward apply pass; z and dz are read by the backward reduce
+// pass and again by the backward apply pass.  z and dx are written for a
+// consumer that runs much later (the backward / the previous layer).
+constexpr int kHintStatsLoad = kCached;
+constexpr int kHintFwdApplyLoad = kStream;
+constexpr int kHintFwdApplyStore = kStream;
+constexpr int kHintReduceLoad = kCached;
+constexpr int kHintBwdApplyLoad = kStream;
+constexpr int kHintBwdApplyStore = kStream;
 
 // ---------------------------------------------------------------- geometry
 
 struct Geom {
     uint32_t C;      // channels
-    uint32_t P;      // slices per channel
+    uint32_t P;      // slices per channel (one block each)
     uint32_t vrow;   // accesses per row (HW / VEC)
     uint32_t vchan;  // accesses per channel (N * vrow)
     uint32_t lv;     // accesses per slice (the last slice may be shorter)
@@ -139,98 +165,84 @@ __device__ __forceinline__ Slice block_slice(const Geom& g) {
     return s;
 }
 
-// Elements in slice p of a channel.
-__device__ __forceinline__ double slice_count(const Geom& g, uint32_t p) {
-    const uint32_t lo = p * g.lv;
-    const uint32_t hi = min(lo + g.lv, g.vchan);
-    return static_cast<double>(hi - lo) * static_cast<double>(g.vec);
-}
+// ---------------------------------------------------------------- partials
 
-// ---------------------------------------------------------------- reductions
-
-// Count, mean and sum of squared deviations of a set of values, in double.
-// Two sets combine with the pairwise update of Chan, Golub and LeVeque
-// (1979).  Per-element work stays in fp32 (see fwd_stats_kernel); only the
-// per-thread results and everything after them are double, which costs a few
-// dozen instructions per thread and keeps large channel means from eating
-// the fp32 mantissa.
-struct Moments {
-    double n, mean, m2;
+// One partial result per wave of a reduction kernel, 32 bytes:
+//   forward:  k, s1 = sum(x - k), s2 = sum((x - k)^2), n   (shifted sums)
+//   backward: sum dy, sum dy*xhat, 0, 0
+// A channel's partials are part[(c*P + p)*kWaves + w].
+struct alignas(16) Partial {
+    double a, b, c, d;
 };
 
-__device__ __forceinline__ Moments chan_merge(const Moments& a, const Moments& b) {
-    const double n = a.n + b.n;
-    const double wb = n > 0.0 ? b.n / n : 0.0;
-    const double d = b.mean - a.mean;
-    Moments r;
-    r.n = n;
-    r.mean = fma(d, wb, a.mean);
-    r.m2 = a.m2 + b.m2 + d * d * a.n * wb;
-    return r;
-}
+__device__ __forceinline__ uint32_t lane_id() { return threadIdx.x & (kWave - 1); }
 
-// Fixed-order tree over a wave; lane 0 ends with the merge of all 64 lanes.
-__device__ __forceinline__ Moments wave_merge(Moments a) {
+__device__ __forceinline__ double wave_sum(double v) {
 #pragma unroll
-    for (int off = kWave / 2; off > 0; off >>= 1) {
-        Moments b;
-        b.n = __shfl_down(a.n, off, kWave);
-        b.mean = __shfl_down(a.mean, off, kWave);
-        b.m2 = __shfl_down(a.m2, off, kWave);
-        if ((threadIdx.x & (kWave - 1)) < static_cast<unsigned>(off)) a = chan_merge(a, b);
-    }
-    return a;
+    for (int off = kWave / 2; off > 0; off >>= 1) v += __shfl_down(v, off, kWave);
+    return v;  // valid in lane 0
 }
 
-__device__ __forceinline__ double2 wave_sum(double2 a) {
-#pragma unroll
-    for (int off = kWave / 2; off > 0; off >>= 1) {
-        a.x += __shfl_down(a.x, off, kWave);
-        a.y += __shfl_down(a.y, off, kWave);
-    }
-    return a;
+// Shifted sums re-expressed about another shift:
+//   sum(x - k') = s1 + n d,  sum((x - k')^2) = s2 + d (2 s1 + n d),  d = k - k'.
+__device__ __forceinline__ void reshift(double& s1, double& s2, double n, double k_from,
+                                        double k_to) {
+    const double d = k_from - k_to;
+    s2 += d * (2.0 * s1 + n * d);
+    s1 += n * d;
 }
 
-// Combine a channel's P partial moments (fixed order); run by one full wave,
-// the result is valid in lane 0.
-__device__ __forceinline__ Moments combine_channel_moments(const Geom& g,
-                                                           const double2* __restrict__ part,
-                                                           uint32_t c) {
-    const uint32_t lane = threadIdx.x & (kWave - 1);
-    Moments acc = {0.0, 0.0, 0.0};
-    for (uint32_t p = lane; p < g.P; p += kWave) {
-        const double2 pm = part[static_cast<uint64_t>(c) * g.P + p];
-        const Moments b = {slice_count(g, p), pm.x, pm.y};
-        acc = chan_merge(acc, b);
+// Batch mean and biased variance of channel c from its P*kWaves partials,
+// combined in a fixed order by every lane of the calling wave (all lanes get
+// the result).  Everything is double: the shift k of the first partial is a
+// value of the channel, so the final cancellation S2 - S1^2/n loses at most a
+// few of double's 53 bits.
+__device__ __forceinline__ void channel_moments(const Geom& g, const Partial* __restrict__ part,
+                                                uint32_t c, double& mean, double& var) {
+    const uint32_t np = g.P * kWaves;
+    const Partial* cp = part + static_cast<uint64_t>(c) * np;
+    const double kref = cp[0].a;
+    double s1 = 0.0, s2 = 0.0, n = 0.0;
+    for (uint32_t q = lane_id(); q < np; q += kWave) {
+        const Partial pq = cp[q];
+        double t1 = pq.b, t2 = pq.c;
+        reshift(t1, t2, pq.d, pq.a, kref);
+        s1 += t1;
+        s2 += t2;
+        n += pq.d;
     }
-    return wave_merge(acc);
+    s1 = __shfl(wave_sum(s1), 0, kWave);
+    s2 = __shfl(wave_sum(s2), 0, kWave);
+    n = __shfl(wave_sum(n), 0, kWave);
+    mean = kref + s1 / n;
+    var = fmax(s2 - s1 * s1 / n, 0.0) / n;
 }
 
-__device__ __forceinline__ double2 combine_channel_sums(const Geom& g,
-                                                        const double2* __restrict__ part,
-                                                        uint32_t c) {
-    const uint32_t lane = threadIdx.x & (kWave - 1);
-    double2 acc = make_double2(0.0, 0.0);
-    for (uint32_t p = lane; p < g.P; p += kWave) {
-        const double2 s = part[static_cast<uint64_t>(c) * g.P + p];
-        acc.x += s.x;
-        acc.y += s.y;
+__device__ __forceinline__ void channel_sums(const Geom& g, const Partial* __restrict__ part,
+                                             uint32_t c, double& sdy, double& sdyx) {
+    const uint32_t np = g.P * kWaves;
+    const Partial* cp = part + static_cast<uint64_t>(c) * np;
+    double a = 0.0, b = 0.0;
+    for (uint32_t q = lane_id(); q < np; q += kWave) {
+        a += cp[q].a;
+        b += cp[q].b;
     }
-    return wave_sum(acc);
+    sdy = __shfl(wave_sum(a), 0, kWave);
+    sdyx = __shfl(wave_sum(b), 0, kWave);
 }
 
 // ---------------------------------------------------------------- forward
 
-// Partial moments of one (channel, slice): part[c*P + p] = (mean, M2).
+// Shifted sums of one wave's share of a (channel, slice).
 //
-// Each thread accumulates shifted sums S1 = sum(x - K), S2 = sum((x - K)^2)
-// in fp32 with K = the first value it reads, which sits within a few standard
-// deviations of the mean, so x - K carries the spread and not the offset
-// (and is exact when x and K are within a factor of two).  The thread's
-// moments are then mean = K + S1/n, M2 = S2 - S1^2/n, formed in double.
+// Each thread accumulates S1 = sum(x - K), S2 = sum((x - K)^2) in fp32 with
+// K = the first value it reads, which sits within a few standard deviations
+// of the mean, so x - K carries the spread and not the offset (and is exact
+// when x and K are within a factor of two).  The thread's sums are then
+// re-expressed about lane 0's K in double and summed over the wave.
 template <int DT, int VEC, int U>
 __global__ __launch_bounds__(kThreads) void fwd_stats_kernel(const void* __restrict__ x, Geom g,
-                                                             double2* __restrict__ part) {
+                                                             Partial* __restrict__ part) {
     const Slice s = block_slice(g);
     const uint64_t cbase = static_cast<uint64_t>(s.c) * g.vrow;
     float shift = 0.f, s1 = 0.f, s2 = 0.f;
@@ -240,7 +252,8 @@ __global__ __launch_bounds__(kThreads) void fwd_stats_kernel(const void* __restr
     for (; v + (U - 1) * kThreads < s.hi; v += U * kThreads) {
         float t[U][VEC];
 #pragma unroll
-        for (int u = 0; u < U; ++u) load_vec<DT, VEC>(x, access_index(g, cbase, v + u * kThreads), t[u]);
+        for (int u = 0; u < U; ++u)
+            load_vec<DT, VEC, kHintStatsLoad>(x, access_index(g, cbase, v + u * kThreads), t[u]);
         if (first) shift = t[0][0];
         first = false;
         float a1 = 0.f, a2 = 0.f;
@@ -259,7 +272,7 @@ __global__ __launch_bounds__(kThreads) void fwd_stats_kernel(const void* __restr
     }
     for (; v < s.hi; v += kThreads) {
         float t[VEC];
-        load_vec<DT, VEC>(x, access_index(g, cbase, v), t);
+        load_vec<DT, VEC, kHintStatsLoad>(x, access_index(g, cbase, v), t);
         if (first) shift = t[0];
         first = false;
 #pragma unroll
@@ -270,25 +283,22 @@ __global__ __launch_bounds__(kThreads) void fwd_stats_kernel(const void* __restr
         }
         nacc += 1;
     }
-    Moments acc = {0.0, 0.0, 0.0};
-    if (nacc > 0) {
-        const double n = static_cast<double>(nacc) * g.vec;
-        const double d1 = s1, d2 = s2;
-        acc.n = n;
-        acc.mean = static_cast<double>(shift) + d1 / n;
-        acc.m2 = fmax(d2 - d1 * d1 / n, 0.0);
-    }
-    acc = wave_merge(acc);
-
-    __shared__ Moments wave_acc[kWaves];
-    const uint32_t wave = threadIdx.x / kWave;
-    if ((threadIdx.x & (kWave - 1)) == 0) wave_acc[wave] = acc;
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        Moments r = wave_acc[0];
-#pragma unroll
-        for (int w = 1; w < kWaves; ++w) r = chan_merge(r, wave_acc[w]);
-        part[static_cast<uint64_t>(s.c) * g.P + s.p] = make_double2(r.mean, r.m2);
+    // Lane 0 has the smallest index of its wave, so if it read nothing the
+    // whole wave read nothing and its sums are zero.
+    const double kw = __shfl(shift, 0, kWave);
+    const double n = static_cast<double>(nacc) * g.vec;
+    double d1 = s1, d2 = s2;
+    reshift(d1, d2, n, shift, kw);
+    d1 = wave_sum(d1);
+    d2 = wave_sum(d2);
+    const double nw = wave_sum(n);
+    if (lane_id() == 0) {
+        Partial r;
+        r.a = kw;
+        r.b = d1;
+        r.c = d2;
+        r.d = nw;
+        part[(static_cast<uint64_t>(s.c) * g.P + s.p) * kWaves + threadIdx.x / kWave] = r;
     }
 }
 
@@ -309,75 +319,79 @@ struct FwdParams {
 // hi + lo, so x - mu keeps fp32 relative accuracy even when |mu| >> sigma.
 template <int DT, int VEC, int U, bool TRAIN>
 __global__ __launch_bounds__(kThreads) void fwd_apply_kernel(void* __restrict__ xz, Geom g,
-                                                             const double2* __restrict__ part,
+                                                             const Partial* __restrict__ part,
                                                              FwdParams prm) {
     const Slice s = block_slice(g);
-    __shared__ float coef[4];
-    if (threadIdx.x < kWave) {
-        double mean, var;
-        if constexpr (TRAIN) {
-            const Moments r = combine_channel_moments(g, part, s.c);
-            mean = r.mean;
-            var = fmax(r.m2, 0.0) / g.m;
-        } else {
-            mean = prm.running_mean[s.c];
-            var = prm.running_var[s.c];
-        }
-        if (threadIdx.x == 0) {
-            const double scale = static_cast<double>(prm.gamma[s.c]) / sqrt(var + static_cast<double>(prm.eps));
-            const float mean_hi = static_cast<float>(mean);
-            coef[0] = mean_hi;
-            coef[1] = static_cast<float>(mean - static_cast<double>(mean_hi));
-            coef[2] = static_cast<float>(scale);
-            coef[3] = prm.beta[s.c];
-            if constexpr (TRAIN) {
-                if (s.p == 0) {
-                    const double mom = prm.momentum;
-                    const double m = g.m;
-                    prm.save_mean[s.c] = mean_hi;
-                    prm.save_var[s.c] = static_cast<float>(var);
-                    prm.running_mean[s.c] = static_cast<float>(
-                        (1.0 - mom) * static_cast<double>(prm.running_mean[s.c]) + mom * mean);
-                    prm.running_var[s.c] = static_cast<float>(
-                        (1.0 - mom) * static_cast<double>(prm.running_var[s.c]) +
-                        mom * var * (m / (m - 1.0)));
-                }
-            }
+    const uint64_t cbase = static_cast<uint64_t>(s.c) * g.vrow;
+
+    // First batch in flight before the per-channel coefficients are known.
+    uint32_t v = s.lo + threadIdx.x;
+    float t[U][VEC];
+    uint64_t idx[U];
+    bool full = v + (U - 1) * kThreads < s.hi;
+    if (full) {
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            idx[u] = access_index(g, cbase, v + u * kThreads);
+            load_vec<DT, VEC, kHintFwdApplyLoad>(xz, idx[u], t[u]);
         }
     }
-    __syncthreads();
-    const float mean_hi = coef[0], mean_lo = coef[1], scale = coef[2], shift = coef[3];
+
+    double mean, var;
+    if constexpr (TRAIN) {
+        channel_moments(g, part, s.c, mean, var);
+    } else {
+        mean = prm.running_mean[s.c];
+        var = prm.running_var[s.c];
+    }
+    const float mean_hi = static_cast<float>(mean);
+    const float mean_lo = static_cast<float>(mean - static_cast<double>(mean_hi));
+    const float scale = static_cast<float>(static_cast<double>(prm.gamma[s.c]) /
+                                           sqrt(var + static_cast<double>(prm.eps)));
+    const float shift = prm.beta[s.c];
     const float slope = prm.slope;
-    const uint64_t cbase = static_cast<uint64_t>(s.c) * g.vrow;
+    if constexpr (TRAIN) {
+        if (s.p == 0 && threadIdx.x == 0) {
+            const double mom = prm.momentum;
+            const double m = g.m;
+            prm.save_mean[s.c] = mean_hi;
+            prm.save_var[s.c] = static_cast<float>(var);
+            prm.running_mean[s.c] = static_cast<float>(
+                (1.0 - mom) * static_cast<double>(prm.running_mean[s.c]) + mom * mean);
+            prm.running_var[s.c] = static_cast<float>(
+                (1.0 - mom) * static_cast<double>(prm.running_var[s.c]) + mom * var * (m / (m - 1.0)));
+        }
+    }
 
     auto act = [&](float xv) {
         const float y = fmaf((xv - mean_hi) - mean_lo, scale, shift);
         return y >= 0.f ? y : slope * y;
     };
 
-    uint32_t v = s.lo + threadIdx.x;
-    for (; v + (U - 1) * kThreads < s.hi; v += U * kThreads) {
-        float t[U][VEC];
-        uint64_t idx[U];
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-            idx[u] = access_index(g, cbase, v + u * kThreads);
-            load_vec<DT, VEC>(xz, idx[u], t[u]);
-        }
+    while (full) {
 #pragma unroll
         for (int u = 0; u < U; ++u) {
 #pragma unroll
             for (int k = 0; k < VEC; ++k) t[u][k] = act(t[u][k]);
-            store_vec<DT, VEC>(xz, idx[u], t[u]);
+            store_vec<DT, VEC, kHintFwdApplyStore>(xz, idx[u], t[u]);
+        }
+        v += U * kThreads;
+        full = v + (U - 1) * kThreads < s.hi;
+        if (full) {
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                idx[u] = access_index(g, cbase, v + u * kThreads);
+                load_vec<DT, VEC, kHintFwdApplyLoad>(xz, idx[u], t[u]);
+            }
         }
     }
     for (; v < s.hi; v += kThreads) {
-        float t[VEC];
-        const uint64_t idx = access_index(g, cbase, v);
-        load_vec<DT, VEC>(xz, idx, t);
+        float r[VEC];
+        const uint64_t i1 = access_index(g, cbase, v);
+        load_vec<DT, VEC, kHintFwdApplyLoad>(xz, i1, r);
 #pragma unroll
-        for (int k = 0; k < VEC; ++k) t[k] = act(t[k]);
-        store_vec<DT, VEC>(xz, idx, t);
+        for (int k = 0; k < VEC; ++k) r[k] = act(r[k]);
+        store_vec<DT, VEC, kHintFwdApplyStore>(xz, i1, r);
     }
 }
 
@@ -397,28 +411,27 @@ struct BwdElem {
     }
 };
 
-// Partial sums of dy and dy*xhat of one (channel, slice):
-// part[c*P + p] = (sum dy, sum dy*xhat).  fp32 per batch of U accesses,
-// double across batches and threads.
+// Sums of dy and dy*xhat of one wave's share of a (channel, slice): fp32 per
+// batch of U accesses, double across batches and lanes.
 template <int DT, int VEC, int U>
 __global__ __launch_bounds__(kThreads) void bwd_reduce_kernel(const void* __restrict__ z,
                                                               const void* __restrict__ dz, Geom g,
                                                               const float* __restrict__ gamma,
                                                               const float* __restrict__ beta,
                                                               float slope,
-                                                              double2* __restrict__ part) {
+                                                              Partial* __restrict__ part) {
     const Slice s = block_slice(g);
     const BwdElem el = {slope, 1.0f / slope, beta[s.c], 1.0f / gamma[s.c]};
     const uint64_t cbase = static_cast<uint64_t>(s.c) * g.vrow;
-    double2 acc = make_double2(0.0, 0.0);
+    double acc_dy = 0.0, acc_dyx = 0.0;
     uint32_t v = s.lo + threadIdx.x;
     for (; v + (U - 1) * kThreads < s.hi; v += U * kThreads) {
         float tz[U][VEC], tg[U][VEC];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            const uint64_t idx = access_index(g, cbase, v + u * kThreads);
-            load_vec<DT, VEC>(z, idx, tz[u]);
-            load_vec<DT, VEC>(dz, idx, tg[u]);
+            const uint64_t i1 = access_index(g, cbase, v + u * kThreads);
+            load_vec<DT, VEC, kHintReduceLoad>(z, i1, tz[u]);
+            load_vec<DT, VEC, kHintReduceLoad>(dz, i1, tg[u]);
         }
         float sdy = 0.f, sdyx = 0.f;
 #pragma unroll
@@ -431,14 +444,14 @@ __global__ __launch_bounds__(kThreads) void bwd_reduce_kernel(const void* __rest
                 sdyx = fmaf(dy, xhat, sdyx);
             }
         }
-        acc.x += sdy;
-        acc.y += sdyx;
+        acc_dy += sdy;
+        acc_dyx += sdyx;
     }
     for (; v < s.hi; v += kThreads) {
         float tz[VEC], tg[VEC];
-        const uint64_t idx = access_index(g, cbase, v);
-        load_vec<DT, VEC>(z, idx, tz);
-        load_vec<DT, VEC>(dz, idx, tg);
+        const uint64_t i1 = access_index(g, cbase, v);
+        load_vec<DT, VEC, kHintReduceLoad>(z, i1, tz);
+        load_vec<DT, VEC, kHintReduceLoad>(dz, i1, tg);
         float sdy = 0.f, sdyx = 0.f;
 #pragma unroll
         for (int k = 0; k < VEC; ++k) {
@@ -447,23 +460,18 @@ __global__ __launch_bounds__(kThreads) void bwd_reduce_kernel(const void* __rest
             sdy += dy;
             sdyx = fmaf(dy, xhat, sdyx);
         }
-        acc.x += sdy;
-        acc.y += sdyx;
+        acc_dy += sdy;
+        acc_dyx += sdyx;
     }
-    acc = wave_sum(acc);
-
-    __shared__ double2 wave_acc[kWaves];
-    const uint32_t wave = threadIdx.x / kWave;
-    if ((threadIdx.x & (kWave - 1)) == 0) wave_acc[wave] = acc;
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        double2 r = wave_acc[0];
-#pragma unroll
-        for (int w = 1; w < kWaves; ++w) {
-            r.x += wave_acc[w].x;
-            r.y += wave_acc[w].y;
-        }
-        part[static_cast<uint64_t>(s.c) * g.P + s.p] = r;
+    acc_dy = wave_sum(acc_dy);
+    acc_dyx = wave_sum(acc_dyx);
+    if (lane_id() == 0) {
+        Partial r;
+        r.a = acc_dy;
+        r.b = acc_dyx;
+        r.c = 0.0;
+        r.d = 0.0;
+        part[(static_cast<uint64_t>(s.c) * g.P + s.p) * kWaves + threadIdx.x / kWave] = r;
     }
 }
 
@@ -481,29 +489,37 @@ struct BwdParams {
 template <int DT, int VEC, int U>
 __global__ __launch_bounds__(kThreads) void bwd_apply_kernel(const void* __restrict__ z,
                                                              void* __restrict__ dzdx, Geom g,
-                                                             const double2* __restrict__ part,
+                                                             const Partial* __restrict__ part,
                                                              BwdParams prm) {
     const Slice s = block_slice(g);
-    __shared__ float coef[3];
-    if (threadIdx.x < kWave) {
-        const double2 sums = combine_channel_sums(g, part, s.c);
-        if (threadIdx.x == 0) {
-            const double dbeta = sums.x, dgamma = sums.y, m = g.m;
-            const double a = static_cast<double>(prm.gamma[s.c]) /
-                             sqrt(static_cast<double>(prm.save_var[s.c]) + static_cast<double>(prm.eps));
-            coef[0] = static_cast<float>(a);
-            coef[1] = static_cast<float>(-a * dgamma / m);
-            coef[2] = static_cast<float>(-a * dbeta / m);
-            if (s.p == 0) {
-                prm.dgamma[s.c] = static_cast<float>(dgamma);
-                prm.dbeta[s.c] = static_cast<float>(dbeta);
-            }
+    const uint64_t cbase = static_cast<uint64_t>(s.c) * g.vrow;
+
+    uint32_t v = s.lo + threadIdx.x;
+    float tz[U][VEC], tg[U][VEC];
+    uint64_t idx[U];
+    bool full = v + (U - 1) * kThreads < s.hi;
+    if (full) {
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            idx[u] = access_index(g, cbase, v + u * kThreads);
+            load_vec<DT, VEC, kHintBwdApplyLoad>(z, idx[u], tz[u]);
+            load_vec<DT, VEC, kHintBwdApplyLoad>(dzdx, idx[u], tg[u]);
         }
     }
-    __syncthreads();
-    const float ca = coef[0], cb = coef[1], cc = coef[2];
+
+    double dbeta, dgamma;
+    channel_sums(g, part, s.c, dbeta, dgamma);
+    const double m = g.m;
+    const double a = static_cast<double>(prm.gamma[s.c]) /
+                     sqrt(static_cast<double>(prm.save_var[s.c]) + static_cast<double>(prm.eps));
+    const float ca = static_cast<float>(a);
+    const float cb = static_cast<float>(-a * dgamma / m);
+    const float cc = static_cast<float>(-a * dbeta / m);
+    if (s.p == 0 && threadIdx.x == 0) {
+        prm.dgamma[s.c] = static_cast<float>(dgamma);
+        prm.dbeta[s.c] = static_cast<float>(dbeta);
+    }
     const BwdElem el = {prm.slope, 1.0f / prm.slope, prm.beta[s.c], 1.0f / prm.gamma[s.c]};
-    const uint64_t cbase = static_cast<uint64_t>(s.c) * g.vrow;
 
     auto dx_of = [&](float zv, float gv) {
         float dy, xhat;
@@ -511,31 +527,32 @@ __global__ __launch_bounds__(kThreads) void bwd_apply_kernel(const void* __restr
         return fmaf(ca, dy, fmaf(cb, xhat, cc));
     };
 
-    uint32_t v = s.lo + threadIdx.x;
-    for (; v + (U - 1) * kThreads < s.hi; v += U * kThreads) {
-        float tz[U][VEC], tg[U][VEC];
-        uint64_t idx[U];
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-            idx[u] = access_index(g, cbase, v + u * kThreads);
-            load_vec<DT, VEC>(z, idx[u], tz[u]);
-            load_vec<DT, VEC>(dzdx, idx[u], tg[u]);
-        }
+    while (full) {
 #pragma unroll
         for (int u = 0; u < U; ++u) {
 #pragma unroll
             for (int k = 0; k < VEC; ++k) tg[u][k] = dx_of(tz[u][k], tg[u][k]);
-            store_vec<DT, VEC>(dzdx, idx[u], tg[u]);
+            store_vec<DT, VEC, kHintBwdApplyStore>(dzdx, idx[u], tg[u]);
+        }
+        v += U * kThreads;
+        full = v + (U - 1) * kThreads < s.hi;
+        if (full) {
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                idx[u] = access_index(g, cbase, v + u * kThreads);
+                load_vec<DT, VEC, kHintBwdApplyLoad>(z, idx[u], tz[u]);
+                load_vec<DT, VEC, kHintBwdApplyLoad>(dzdx, idx[u], tg[u]);
+            }
         }
     }
     for (; v < s.hi; v += kThreads) {
-        float tz[VEC], tg[VEC];
-        const uint64_t idx = access_index(g, cbase, v);
-        load_vec<DT, VEC>(z, idx, tz);
-        load_vec<DT, VEC>(dzdx, idx, tg);
+        float rz[VEC], rg[VEC];
+        const uint64_t i1 = access_index(g, cbase, v);
+        load_vec<DT, VEC, kHintBwdApplyLoad>(z, i1, rz);
+        load_vec<DT, VEC, kHintBwdApplyLoad>(dzdx, i1, rg);
 #pragma unroll
-        for (int k = 0; k < VEC; ++k) tg[k] = dx_of(tz[k], tg[k]);
-        store_vec<DT, VEC>(dzdx, idx, tg);
+        for (int k = 0; k < VEC; ++k) rg[k] = dx_of(rz[k], rg[k]);
+        store_vec<DT, VEC, kHintBwdApplyStore>(dzdx, i1, rg);
     }
 }
 
@@ -606,7 +623,7 @@ int check_shape(int64_t N, int64_t C, int64_t HW, bool train) {
 size_t workspace_bytes_for(int64_t N, int64_t C, int64_t HW) {
     if (C == 0 || N * HW == 0) return 0;
     const Split sp = split_channel(N * HW, C);
-    return static_cast<size_t>(C) * static_cast<size_t>(sp.P) * sizeof(double2);
+    return static_cast<size_t>(C) * static_cast<size_t>(sp.P) * kWaves * sizeof(Partial);
 }
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
@@ -689,14 +706,14 @@ constexpr int unroll() {
 
 template <int DT, int VEC>
 struct LaunchFwdStats {
-    static void run(const void* x, const Geom& g, double2* part, hipStream_t st) {
+    static void run(const void* x, const Geom& g, Partial* part, hipStream_t st) {
         fwd_stats_kernel<DT, VEC, unroll<VEC>()><<<grid_of(g), kThreads, 0, st>>>(x, g, part);
     }
 };
 
 template <int DT, int VEC>
 struct LaunchFwdApply {
-    static void run(void* xz, const Geom& g, const double2* part, const FwdParams& prm, bool train,
+    static void run(void* xz, const Geom& g, const Partial* part, const FwdParams& prm, bool train,
                     hipStream_t st) {
         if (train)
             fwd_apply_kernel<DT, VEC, unroll<VEC>(), true><<<grid_of(g), kThreads, 0, st>>>(
@@ -710,7 +727,7 @@ struct LaunchFwdApply {
 template <int DT, int VEC>
 struct LaunchBwdReduce {
     static void run(const void* z, const void* dz, const Geom& g, const float* gamma,
-                    const float* beta, float slope, double2* part, hipStream_t st) {
+                    const float* beta, float slope, Partial* part, hipStream_t st) {
         bwd_reduce_kernel<DT, VEC, unroll<VEC>()><<<grid_of(g), kThreads, 0, st>>>(
             z, dz, g, gamma, beta, slope, part);
     }
@@ -718,7 +735,7 @@ struct LaunchBwdReduce {
 
 template <int DT, int VEC>
 struct LaunchBwdApply {
-    static void run(const void* z, void* dzdx, const Geom& g, const double2* part,
+    static void run(const void* z, void* dzdx, const Geom& g, const Partial* part,
                     const BwdParams& prm, hipStream_t st) {
         bwd_apply_kernel<DT, VEC, unroll<VEC>()><<<grid_of(g), kThreads, 0, st>>>(z, dzdx, g,
                                                                                    part, prm);
@@ -770,7 +787,7 @@ int iabn_forward_stats(const void* x, int dtype, int64_t N, int64_t C, int64_t H
     if ((rc = check_workspace(N, C, HW, workspace, workspace_bytes))) return rc;
     const bool vec = use_vector(HW, dtype, x, nullptr);
     const Geom g = make_geom(N, C, HW, dtype, vec);
-    dispatch<LaunchFwdStats>(dtype, vec, x, g, static_cast<double2*>(workspace),
+    dispatch<LaunchFwdStats>(dtype, vec, x, g, static_cast<Partial*>(workspace),
                              static_cast<hipStream_t>(stream));
     return launched("fwd_stats");
 }
@@ -793,7 +810,7 @@ int iabn_forward_apply(void* x_z, int dtype, const float* gamma, const float* be
     const Geom g = make_geom(N, C, HW, dtype, vec);
     const FwdParams prm = {gamma, beta, running_mean, running_var, save_mean, save_var,
                            eps,   momentum, slope};
-    dispatch<LaunchFwdApply>(dtype, vec, x_z, g, static_cast<const double2*>(workspace), prm, true,
+    dispatch<LaunchFwdApply>(dtype, vec, x_z, g, static_cast<const Partial*>(workspace), prm, true,
                              static_cast<hipStream_t>(stream));
     return launched("fwd_apply");
 }
@@ -833,7 +850,7 @@ int iabn_forward_eval(void* x_z, int dtype, const float* gamma, const float* bet
     const Geom g = make_geom(N, C, HW, dtype, vec);
     const FwdParams prm = {gamma, beta, const_cast<float*>(running_mean),
                            const_cast<float*>(running_var), nullptr, nullptr, eps, 0.f, slope};
-    dispatch<LaunchFwdApply>(dtype, vec, x_z, g, static_cast<const double2*>(nullptr), prm, false,
+    dispatch<LaunchFwdApply>(dtype, vec, x_z, g, static_cast<const Partial*>(nullptr), prm, false,
                              static_cast<hipStream_t>(stream));
     return launched("fwd_eval");
 }
@@ -852,7 +869,7 @@ int iabn_backward_reduce(const void* z, const void* dz, int dtype, const float* 
     const bool vec = use_vector(HW, dtype, z, dz);
     const Geom g = make_geom(N, C, HW, dtype, vec);
     dispatch<LaunchBwdReduce>(dtype, vec, z, dz, g, gamma, beta, slope,
-                              static_cast<double2*>(workspace), static_cast<hipStream_t>(stream));
+                              static_cast<Partial*>(workspace), static_cast<hipStream_t>(stream));
     return launched("bwd_reduce");
 }
 
@@ -870,7 +887,7 @@ int iabn_backward_apply(const void* z, void* dz_dx, int dtype, const float* gamm
     const bool vec = use_vector(HW, dtype, z, dz_dx);
     const Geom g = make_geom(N, C, HW, dtype, vec);
     const BwdParams prm = {gamma, beta, save_var, dgamma, dbeta, eps, slope};
-    dispatch<LaunchBwdApply>(dtype, vec, z, dz_dx, g, static_cast<const double2*>(workspace), prm,
+    dispatch<LaunchBwdApply>(dtype, vec, z, dz_dx, g, static_cast<const Partial*>(workspace), prm,
                              static_cast<hipStream_t>(stream));
     return launched("bwd_apply");
 }

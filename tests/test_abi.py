@@ -79,7 +79,7 @@ def _split(m, C):
                                     (8, 1024, 4096), (8, 2048, 4096), (3, 5, 7), (1, 1, 2)])
 def test_workspace_size(lib, N, C, HW):
     for dt in (F32, F16, BF16):
-        assert lib.iabn_workspace_size(N, C, HW, dt) == C * _split(N * HW, C) * 16
+        assert lib.iabn_workspace_size(N, C, HW, dt) == C * _split(N * HW, C) * 4 * 32
 
 
 def test_workspace_size_invalid(lib):
