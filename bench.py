@@ -74,13 +74,19 @@ def main():
         print("bench.py runs as a single process on one GPU", file=sys.stderr)
         sys.exit(2)
 
+    import paper_1712_02616_amd as iabn
+
+    print(json.dumps(measure(iabn.load(), args)), flush=True)
+
+
+def measure(lib, args):
+    """Run the benchmark with a loaded libiabn handle; returns the JSON record."""
     import numpy as np
     import torch
 
     import paper_1712_02616_amd as iabn
     import workloads
 
-    lib = iabn.load()
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     w = workloads.WORKLOADS[args.config]
@@ -297,7 +303,7 @@ def main():
         "roofline": roofline,
         "cpu_baseline": cpu,
     }
-    print(json.dumps(out), flush=True)
+    return out
 
 
 if __name__ == "__main__":

@@ -54,7 +54,12 @@ def load():
         return _lib
     if not _build.is_built():
         _build.build()
-    lib = ctypes.CDLL(_build.LIB)
+    _lib = declare(ctypes.CDLL(_build.LIB))
+    return _lib
+
+
+def declare(lib):
+    """Attach the C signatures of include/iabn.h to a loaded libiabn handle."""
     vp, i64, f32, sz, i32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_float, ctypes.c_size_t, ctypes.c_int
     sig = {
         "iabn_version": ([], i32),
@@ -73,7 +78,6 @@ def load():
         fn = getattr(lib, name)
         fn.argtypes = args
         fn.restype = res
-    _lib = lib
     return lib
 
 

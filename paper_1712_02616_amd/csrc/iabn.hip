@@ -130,6 +130,8 @@ constexpr int kHintFwdApplyStore = kStream;
 constexpr int kHintReduceLoad = kCached;
 constexpr int kHintBwdApplyLoad = kStream;
 constexpr int kHintBwdApplyStore = kStream;
+// Apply passes visit the slices in reverse order of their reduction pass.
+constexpr bool kReverseApply = false;
 
 // ---------------------------------------------------------------- geometry
 
@@ -156,10 +158,15 @@ struct Slice {
     uint32_t c, p, lo, hi;
 };
 
+// REVERSE walks the slices from the last to the first: an apply pass then
+// starts on the data its reduction pass fetched most recently, which is the
+// data most likely still in the caches.
+template <bool REVERSE = false>
 __device__ __forceinline__ Slice block_slice(const Geom& g) {
     Slice s;
-    s.c = blockIdx.x / g.P;
-    s.p = blockIdx.x - s.c * g.P;
+    const uint32_t b = REVERSE ? gridDim.x - 1 - blockIdx.x : blockIdx.x;
+    s.c = b / g.P;
+    s.p = b - s.c * g.P;
     s.lo = s.p * g.lv;
     s.hi = min(s.lo + g.lv, g.vchan);
     return s;
@@ -321,7 +328,7 @@ template <int DT, int VEC, int U, bool TRAIN>
 __global__ __launch_bounds__(kThreads) void fwd_apply_kernel(void* __restrict__ xz, Geom g,
                                                              const Partial* __restrict__ part,
                                                              FwdParams prm) {
-    const Slice s = block_slice(g);
+    const Slice s = block_slice<kReverseApply>(g);
     const uint64_t cbase = static_cast<uint64_t>(s.c) * g.vrow;
 
     // First batch in flight before the per-channel coefficients are known.
@@ -491,7 +498,7 @@ __global__ __launch_bounds__(kThreads) void bwd_apply_kernel(const void* __restr
                                                              void* __restrict__ dzdx, Geom g,
                                                              const Partial* __restrict__ part,
                                                              BwdParams prm) {
-    const Slice s = block_slice(g);
+    const Slice s = block_slice<kReverseApply>(g);
     const uint64_t cbase = static_cast<uint64_t>(s.c) * g.vrow;
 
     uint32_t v = s.lo + threadIdx.x;
@@ -556,6 +563,326 @@ __global__ __launch_bounds__(kThreads) void bwd_apply_kernel(const void* __restr
     }
 }
 
+// ---------------------------------------------------------------- fused, channel-resident
+
+// One block owns a whole channel and keeps the first R of each thread's
+// 16-byte accesses in registers between the reduction and the apply phase,
+// so those bytes cross HBM once on the way in and once on the way out (the
+// forward reads x and writes z; the backward reads z and dz and writes dx).
+// Accesses beyond R (channels larger than the block's registers) are read
+// again in the apply phase.  Thread t handles accesses t, t + T, t + 2T, ...
+// of its channel, so a wave touches consecutive 16-byte vectors.  The only
+// synchronisation is the block barrier around the channel's reduction.
+
+typedef uint32_t raw16_t __attribute__((ext_vector_type(4)));
+
+// Hide a value from the optimiser (an empty asm that "may change" it).  Used
+// after the reduction barrier so that the apply phase keeps only the raw
+// 16-byte registers alive and converts them again, instead of keeping the
+// twice-as-large fp32 values (and 64-bit addresses) from the first phase.
+template <typename V>
+__device__ __forceinline__ void opaque(V& v) {
+    asm volatile("" : "+v"(v));
+}
+
+template <int HINT>
+__device__ __forceinline__ raw16_t load_raw(const void* __restrict__ base, uint64_t idx) {
+    const raw16_t* p = static_cast<const raw16_t*>(base) + idx;
+    return HINT == kStream ? __builtin_nontemporal_load(p) : *p;
+}
+
+template <int DT, int VEC>
+__device__ __forceinline__ void unpack(raw16_t r, float (&v)[VEC]) {
+    using T = typename Elem<DT>::T;
+    typedef T vt __attribute__((ext_vector_type(VEC)));
+    typedef float vf __attribute__((ext_vector_type(VEC)));
+    const vf f = __builtin_convertvector(__builtin_bit_cast(vt, r), vf);
+#pragma unroll
+    for (int k = 0; k < VEC; ++k) v[k] = f[k];
+}
+
+// Per-wave (shift, s1, s2, n) of a block, combined by wave 0 in a fixed
+// order into the channel's mean and biased variance.
+template <int T>
+__device__ __forceinline__ void block_moments(float shift, float s1, float s2, uint32_t nacc,
+                                              uint32_t vec, double& mean, double& var) {
+    constexpr int W = T / kWave;
+    __shared__ double red[W][4];
+    __shared__ double out[2];
+    const double kw = __shfl(shift, 0, kWave);
+    const double n = static_cast<double>(nacc) * vec;
+    double d1 = s1, d2 = s2;
+    reshift(d1, d2, n, shift, kw);
+    d1 = wave_sum(d1);
+    d2 = wave_sum(d2);
+    const double nw = wave_sum(n);
+    const uint32_t wave = threadIdx.x / kWave;
+    if (lane_id() == 0) {
+        red[wave][0] = kw;
+        red[wave][1] = d1;
+        red[wave][2] = d2;
+        red[wave][3] = nw;
+    }
+    __syncthreads();
+    if (wave == 0) {
+        const double kref = red[0][0];
+        double t1 = 0.0, t2 = 0.0, tn = 0.0;
+        if (lane_id() < W) {
+            t1 = red[lane_id()][1];
+            t2 = red[lane_id()][2];
+            tn = red[lane_id()][3];
+            reshift(t1, t2, tn, red[lane_id()][0], kref);
+        }
+        t1 = wave_sum(t1);
+        t2 = wave_sum(t2);
+        tn = wave_sum(tn);
+        if (lane_id() == 0) {
+            out[0] = kref + t1 / tn;
+            out[1] = fmax(t2 - t1 * t1 / tn, 0.0) / tn;
+        }
+    }
+    __syncthreads();
+    mean = out[0];
+    var = out[1];
+}
+
+template <int T>
+__device__ __forceinline__ void block_sums(double a, double b, double& sa, double& sb) {
+    constexpr int W = T / kWave;
+    __shared__ double red[W][2];
+    __shared__ double out[2];
+    a = wave_sum(a);
+    b = wave_sum(b);
+    const uint32_t wave = threadIdx.x / kWave;
+    if (lane_id() == 0) {
+        red[wave][0] = a;
+        red[wave][1] = b;
+    }
+    __syncthreads();
+    if (wave == 0) {
+        double t1 = lane_id() < W ? red[lane_id()][0] : 0.0;
+        double t2 = lane_id() < W ? red[lane_id()][1] : 0.0;
+        t1 = wave_sum(t1);
+        t2 = wave_sum(t2);
+        if (lane_id() == 0) {
+            out[0] = t1;
+            out[1] = t2;
+        }
+    }
+    __syncthreads();
+    sa = out[0];
+    sb = out[1];
+}
+
+// Training forward of one channel per block (statistics, running estimates,
+// z over x), same arithmetic as fwd_stats_kernel + fwd_apply_kernel.
+template <int DT, int VEC, int T, int R>
+__global__ __launch_bounds__(T) void fwd_fused_kernel(void* __restrict__ xz, Geom g,
+                                                      FwdParams prm) {
+    const uint32_t c = blockIdx.x;
+    const uint64_t cbase = static_cast<uint64_t>(c) * g.vrow;
+    const uint32_t tid = threadIdx.x;
+
+    raw16_t keep[R];
+#pragma unroll
+    for (int k = 0; k < R; ++k) {
+        const uint32_t v = tid + k * T;
+        if (v < g.vchan) keep[k] = load_raw<kCached>(xz, access_index(g, cbase, v));
+    }
+    float shift = 0.f, s1 = 0.f, s2 = 0.f;
+    uint32_t nacc = 0;
+    if (tid < g.vchan) {
+        float t[VEC];
+        unpack<DT, VEC>(keep[0], t);
+        shift = t[0];
+    }
+#pragma unroll
+    for (int k = 0; k < R; ++k) {
+        const uint32_t v = tid + k * T;
+        if (v < g.vchan) {
+            float t[VEC];
+            unpack<DT, VEC>(keep[k], t);
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) {
+                const float d = t[e] - shift;
+                s1 += d;
+                s2 = fmaf(d, d, s2);
+            }
+            ++nacc;
+        }
+    }
+#pragma unroll 1
+    for (uint32_t v = tid + R * T; v < g.vchan; v += T) {
+        float t[VEC];
+        unpack<DT, VEC>(load_raw<kCached>(xz, access_index(g, cbase, v)), t);
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) {
+            const float d = t[e] - shift;
+            s1 += d;
+            s2 = fmaf(d, d, s2);
+        }
+        ++nacc;
+    }
+
+    double mean, var;
+    block_moments<T>(shift, s1, s2, nacc, VEC, mean, var);
+    uint32_t tid2 = tid;
+    opaque(tid2);
+#pragma unroll
+    for (int k = 0; k < R; ++k) opaque(keep[k]);
+    const float mean_hi = static_cast<float>(mean);
+    const float mean_lo = static_cast<float>(mean - static_cast<double>(mean_hi));
+    const float scale = static_cast<float>(static_cast<double>(prm.gamma[c]) /
+                                           sqrt(var + static_cast<double>(prm.eps)));
+    const float bshift = prm.beta[c];
+    const float slope = prm.slope;
+    if (tid == 0) {
+        const double mom = prm.momentum;
+        const double m = g.m;
+        prm.save_mean[c] = mean_hi;
+        prm.save_var[c] = static_cast<float>(var);
+        prm.running_mean[c] = static_cast<float>(
+            (1.0 - mom) * static_cast<double>(prm.running_mean[c]) + mom * mean);
+        prm.running_var[c] = static_cast<float>(
+            (1.0 - mom) * static_cast<double>(prm.running_var[c]) + mom * var * (m / (m - 1.0)));
+    }
+    auto act = [&](float xv) {
+        const float y = fmaf((xv - mean_hi) - mean_lo, scale, bshift);
+        return y >= 0.f ? y : slope * y;
+    };
+
+#pragma unroll
+    for (int k = 0; k < R; ++k) {
+        const uint32_t v = tid2 + k * T;
+        if (v < g.vchan) {
+            float t[VEC];
+            unpack<DT, VEC>(keep[k], t);
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) t[e] = act(t[e]);
+            store_vec<DT, VEC, kHintFwdApplyStore>(xz, access_index(g, cbase, v), t);
+        }
+    }
+#pragma unroll 1
+    for (uint32_t v = tid2 + R * T; v < g.vchan; v += T) {
+        float t[VEC];
+        const uint64_t i1 = access_index(g, cbase, v);
+        unpack<DT, VEC>(load_raw<kStream>(xz, i1), t);
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) t[e] = act(t[e]);
+        store_vec<DT, VEC, kHintFwdApplyStore>(xz, i1, t);
+    }
+}
+
+// Backward of one channel per block (sums of dy and dy*xhat, dgamma, dbeta,
+// dx over dz), same arithmetic as bwd_reduce_kernel + bwd_apply_kernel.
+template <int DT, int VEC, int T, int R>
+__global__ __launch_bounds__(T) void bwd_fused_kernel(const void* __restrict__ z,
+                                                      void* __restrict__ dzdx, Geom g,
+                                                      BwdParams prm) {
+    const uint32_t c = blockIdx.x;
+    const uint64_t cbase = static_cast<uint64_t>(c) * g.vrow;
+    const uint32_t tid = threadIdx.x;
+    const BwdElem el = {prm.slope, 1.0f / prm.slope, prm.beta[c], 1.0f / prm.gamma[c]};
+
+    raw16_t kz[R], kg[R];
+#pragma unroll
+    for (int k = 0; k < R; ++k) {
+        const uint32_t v = tid + k * T;
+        if (v < g.vchan) {
+            const uint64_t i1 = access_index(g, cbase, v);
+            kz[k] = load_raw<kCached>(z, i1);
+            kg[k] = load_raw<kCached>(dzdx, i1);
+        }
+    }
+    double acc_dy = 0.0, acc_dyx = 0.0;
+    {
+        float sdy = 0.f, sdyx = 0.f;
+#pragma unroll
+        for (int k = 0; k < R; ++k) {
+            const uint32_t v = tid + k * T;
+            if (v < g.vchan) {
+                float tz[VEC], tg[VEC];
+                unpack<DT, VEC>(kz[k], tz);
+                unpack<DT, VEC>(kg[k], tg);
+#pragma unroll
+                for (int e = 0; e < VEC; ++e) {
+                    float dy, xhat;
+                    el(tz[e], tg[e], dy, xhat);
+                    sdy += dy;
+                    sdyx = fmaf(dy, xhat, sdyx);
+                }
+            }
+        }
+        acc_dy = sdy;
+        acc_dyx = sdyx;
+    }
+#pragma unroll 1
+    for (uint32_t v = tid + R * T; v < g.vchan; v += T) {
+        float tz[VEC], tg[VEC];
+        const uint64_t i1 = access_index(g, cbase, v);
+        unpack<DT, VEC>(load_raw<kCached>(z, i1), tz);
+        unpack<DT, VEC>(load_raw<kCached>(dzdx, i1), tg);
+        float sdy = 0.f, sdyx = 0.f;
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) {
+            float dy, xhat;
+            el(tz[e], tg[e], dy, xhat);
+            sdy += dy;
+            sdyx = fmaf(dy, xhat, sdyx);
+        }
+        acc_dy += sdy;
+        acc_dyx += sdyx;
+    }
+
+    double dbeta, dgamma;
+    block_sums<T>(acc_dy, acc_dyx, dbeta, dgamma);
+    uint32_t tid2 = tid;
+    opaque(tid2);
+#pragma unroll
+    for (int k = 0; k < R; ++k) {
+        opaque(kz[k]);
+        opaque(kg[k]);
+    }
+    const double m = g.m;
+    const double a = static_cast<double>(prm.gamma[c]) /
+                     sqrt(static_cast<double>(prm.save_var[c]) + static_cast<double>(prm.eps));
+    const float ca = static_cast<float>(a);
+    const float cb = static_cast<float>(-a * dgamma / m);
+    const float cc = static_cast<float>(-a * dbeta / m);
+    if (tid == 0) {
+        prm.dgamma[c] = static_cast<float>(dgamma);
+        prm.dbeta[c] = static_cast<float>(dbeta);
+    }
+    auto dx_of = [&](float zv, float gv) {
+        float dy, xhat;
+        el(zv, gv, dy, xhat);
+        return fmaf(ca, dy, fmaf(cb, xhat, cc));
+    };
+
+#pragma unroll
+    for (int k = 0; k < R; ++k) {
+        const uint32_t v = tid2 + k * T;
+        if (v < g.vchan) {
+            float tz[VEC], tg[VEC];
+            unpack<DT, VEC>(kz[k], tz);
+            unpack<DT, VEC>(kg[k], tg);
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) tg[e] = dx_of(tz[e], tg[e]);
+            store_vec<DT, VEC, kHintBwdApplyStore>(dzdx, access_index(g, cbase, v), tg);
+        }
+    }
+#pragma unroll 1
+    for (uint32_t v = tid2 + R * T; v < g.vchan; v += T) {
+        float tz[VEC], tg[VEC];
+        const uint64_t i1 = access_index(g, cbase, v);
+        unpack<DT, VEC>(load_raw<kStream>(z, i1), tz);
+        unpack<DT, VEC>(load_raw<kStream>(dzdx, i1), tg);
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) tg[e] = dx_of(tz[e], tg[e]);
+        store_vec<DT, VEC, kHintBwdApplyStore>(dzdx, i1, tg);
+    }
+}
+
 // ---------------------------------------------------------------- host side
 
 thread_local char g_last_error[256] = "";
@@ -577,7 +904,7 @@ int ok() {
 constexpr int64_t kMaxChannelElems = (int64_t(1) << 31) - 1;
 constexpr int64_t kMaxChannels = int64_t(1) << 20;
 constexpr int64_t kMaxTotalElems = int64_t(1) << 46;
-constexpr int64_t kTargetBlocks = 2048;    // 8 blocks of 4 waves per CU on 256 CUs
+constexpr int64_t kTargetBlocks = 512;     // 2 blocks of 4 waves per CU on 256 CUs (measured best)
 constexpr int64_t kMinSliceElems = 4096;   // at least 16 elements per thread
 constexpr int64_t kMaxSlices = 1024;
 constexpr int64_t kSliceAlign = 8;         // slices start on a 16-byte access of any dtype
@@ -697,11 +1024,11 @@ void dispatch(int dtype, bool vector, A&&... args) {
     }
 }
 
-// Accesses in flight per thread: 4 x 16 bytes on the vector path, 8 single
-// elements on the scalar path.
+// Accesses in flight per thread and batch: 2 x 16 bytes on the vector path
+// (measured best on the backbone sweep), 8 single elements on the scalar path.
 template <int VEC>
 constexpr int unroll() {
-    return VEC == 1 ? 8 : 4;
+    return VEC == 1 ? 8 : 2;
 }
 
 template <int DT, int VEC>
@@ -741,6 +1068,60 @@ struct LaunchBwdApply {
                                                                                    part, prm);
     }
 };
+
+// ---- fused (channel-resident) path
+
+// Used when every channel gets a block of its own and at least one block per
+// CU (C >= kFusedMinChannels) on the 16-byte path.
+constexpr int64_t kFusedMinChannels = 256;
+
+struct FusedPlan {
+    int T;  // threads per block
+    int R;  // 16-byte accesses per thread held in registers (per tensor)
+};
+
+// The first of (T, R) = (256, 4), (512, 4), (256, 16), (512, 16) whose
+// threads hold the whole channel; larger channels take 1024 threads with
+// R = 16 (forward) or 8 (backward, two tensors) and re-read the remainder.
+bool plan_fused(int64_t C, const Geom& g, bool vector, bool backward, FusedPlan* out) {
+    if (!vector || C < kFusedMinChannels) return false;
+    const int64_t A = g.vchan;
+    const FusedPlan ladder[4] = {{256, 4}, {512, 4}, {256, 16}, {512, 16}};
+    for (const FusedPlan& fp : ladder) {
+        if (A <= static_cast<int64_t>(fp.T) * fp.R) {
+            *out = fp;
+            return true;
+        }
+    }
+    *out = {1024, backward ? 8 : 16};
+    return true;
+}
+
+template <int DT>
+void launch_fwd_fused(void* xz, const Geom& g, const FusedPlan& fp, const FwdParams& prm,
+                      hipStream_t st) {
+    constexpr int V = 16 / sizeof(typename Elem<DT>::T);
+    const dim3 grid(g.C);
+    if (fp.T == 256 && fp.R == 4) fwd_fused_kernel<DT, V, 256, 4><<<grid, 256, 0, st>>>(xz, g, prm);
+    else if (fp.T == 512 && fp.R == 4) fwd_fused_kernel<DT, V, 512, 4><<<grid, 512, 0, st>>>(xz, g, prm);
+    else if (fp.T == 256) fwd_fused_kernel<DT, V, 256, 16><<<grid, 256, 0, st>>>(xz, g, prm);
+    else if (fp.T == 512) fwd_fused_kernel<DT, V, 512, 16><<<grid, 512, 0, st>>>(xz, g, prm);
+    else fwd_fused_kernel<DT, V, 1024, 16><<<grid, 1024, 0, st>>>(xz, g, prm);
+}
+
+template <int DT>
+void launch_bwd_fused(const void* z, void* dzdx, const Geom& g, const FusedPlan& fp,
+                      const BwdParams& prm, hipStream_t st) {
+    constexpr int V = 16 / sizeof(typename Elem<DT>::T);
+    const dim3 grid(g.C);
+    if (fp.T == 256 && fp.R == 4) bwd_fused_kernel<DT, V, 256, 4><<<grid, 256, 0, st>>>(z, dzdx, g, prm);
+    else if (fp.T == 512 && fp.R == 4) bwd_fused_kernel<DT, V, 512, 4><<<grid, 512, 0, st>>>(z, dzdx, g, prm);
+    else if (fp.T == 256) bwd_fused_kernel<DT, V, 256, 16><<<grid, 256, 0, st>>>(z, dzdx, g, prm);
+    else if (fp.T == 512) bwd_fused_kernel<DT, V, 512, 16><<<grid, 512, 0, st>>>(z, dzdx, g, prm);
+    else bwd_fused_kernel<DT, V, 1024, 8><<<grid, 1024, 0, st>>>(z, dzdx, g, prm);
+}
+
+// ---- end fused planning
 
 int validate_common(int dtype, int64_t N, int64_t C, int64_t HW, bool train) {
     if (!valid_dtype(dtype)) return fail(IABN_ERR_DTYPE, "unknown dtype %d", dtype);
@@ -830,6 +1211,18 @@ int iabn_forward_train(void* x_z, int dtype, const float* gamma, const float* be
     if (!(momentum >= 0.f && momentum <= 1.f))
         return fail(IABN_ERR_PARAM, "momentum must lie in [0, 1]");
     if ((rc = check_workspace(N, C, HW, workspace, workspace_bytes))) return rc;
+    const bool vec = use_vector(HW, dtype, x_z, nullptr);
+    const Geom g = make_geom(N, C, HW, dtype, vec);
+    FusedPlan fp;
+    if (plan_fused(C, g, vec, false, &fp)) {
+        const FwdParams prm = {gamma, beta, running_mean, running_var, save_mean, save_var,
+                               eps,   momentum, slope};
+        const hipStream_t st = static_cast<hipStream_t>(stream);
+        if (dtype == IABN_F32) launch_fwd_fused<IABN_F32>(x_z, g, fp, prm, st);
+        else if (dtype == IABN_F16) launch_fwd_fused<IABN_F16>(x_z, g, fp, prm, st);
+        else launch_fwd_fused<IABN_BF16>(x_z, g, fp, prm, st);
+        return launched("fwd_fused");
+    }
     if ((rc = iabn_forward_stats(x_z, dtype, N, C, HW, workspace, workspace_bytes, stream)))
         return rc;
     return iabn_forward_apply(x_z, dtype, gamma, beta, running_mean, running_var, save_mean,
@@ -903,6 +1296,17 @@ int iabn_backward(const void* z, void* dz_dx, int dtype, const float* gamma, con
         return fail(IABN_ERR_NULL, "a tensor or parameter pointer is NULL");
     if ((rc = check_params(eps, slope))) return rc;
     if ((rc = check_workspace(N, C, HW, workspace, workspace_bytes))) return rc;
+    const bool vec = use_vector(HW, dtype, z, dz_dx);
+    const Geom g = make_geom(N, C, HW, dtype, vec);
+    FusedPlan fp;
+    if (plan_fused(C, g, vec, true, &fp)) {
+        const BwdParams prm = {gamma, beta, save_var, dgamma, dbeta, eps, slope};
+        const hipStream_t st = static_cast<hipStream_t>(stream);
+        if (dtype == IABN_F32) launch_bwd_fused<IABN_F32>(z, dz_dx, g, fp, prm, st);
+        else if (dtype == IABN_F16) launch_bwd_fused<IABN_F16>(z, dz_dx, g, fp, prm, st);
+        else launch_bwd_fused<IABN_BF16>(z, dz_dx, g, fp, prm, st);
+        return launched("bwd_fused");
+    }
     if ((rc = iabn_backward_reduce(z, dz_dx, dtype, gamma, beta, slope, N, C, HW, workspace,
                                    workspace_bytes, stream)))
         return rc;

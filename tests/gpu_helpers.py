@@ -80,12 +80,26 @@ class GpuLayer:
         self.workspace = torch.empty(max(iabn.iabn_workspace_size(N, C, HW, TORCH_DTYPES[inp.dtype]), 1),
                                      dtype=torch.uint8, device=device)
 
-    def forward_train(self, eps, momentum, slope):
-        iabn.iabn_forward_train(self.x, self.gamma, self.beta, self.running_mean, self.running_var,
-                                self.save_mean, self.save_var, eps, momentum, slope,
-                                workspace=self.workspace)
+    def forward_train(self, eps, momentum, slope, path="entry"):
+        """path "entry": iabn_forward_train (which may pick the channel-resident
+        kernel); "phases": iabn_forward_stats + iabn_forward_apply."""
+        if path == "entry":
+            iabn.iabn_forward_train(self.x, self.gamma, self.beta, self.running_mean,
+                                    self.running_var, self.save_mean, self.save_var, eps, momentum,
+                                    slope, workspace=self.workspace)
+        else:
+            iabn.iabn_forward_stats(self.x, self.workspace)
+            iabn.iabn_forward_apply(self.x, self.gamma, self.beta, self.running_mean,
+                                    self.running_var, self.save_mean, self.save_var, eps, momentum,
+                                    slope, self.workspace)
 
-    def backward(self, eps, slope, z=None, save_var=None):
-        iabn.iabn_backward(self.x if z is None else z, self.dz, self.gamma, self.beta,
-                           self.save_var if save_var is None else save_var, self.dgamma,
-                           self.dbeta, eps, slope, workspace=self.workspace)
+    def backward(self, eps, slope, z=None, save_var=None, path="entry"):
+        z = self.x if z is None else z
+        sv = self.save_var if save_var is None else save_var
+        if path == "entry":
+            iabn.iabn_backward(z, self.dz, self.gamma, self.beta, sv, self.dgamma, self.dbeta, eps,
+                               slope, workspace=self.workspace)
+        else:
+            iabn.iabn_backward_reduce(z, self.dz, self.gamma, self.beta, slope, self.workspace)
+            iabn.iabn_backward_apply(z, self.dz, self.gamma, self.beta, sv, self.dgamma, self.dbeta,
+                                     eps, slope, self.workspace)

@@ -63,10 +63,10 @@ def test_version_and_status_strings(lib):
 
 
 def _split(m, C):
-    # The slicing rule documented in the library: about 2048 blocks, at
+    # The slicing rule documented in the library: about 512 blocks, at
     # least 4096 elements per slice, at most 1024 slices, slice length a
     # multiple of 8 elements.
-    P = -(-2048 // C)
+    P = -(-512 // C)
     P = min(P, -(-m // 4096), 1024)
     P = max(P, 1)
     L = -(-m // P)

@@ -5,6 +5,11 @@ bit-identically in their storage format; expected values come only from
 ``oracle``.  Gates (max relative error with a floor of 1e-3 * max|ref|):
 1e-4 for fp32 storage, 2e-2 for fp16/bf16 storage with fp32 arithmetic.
 
+Each comparison runs through both ways into the library: the fused entry
+points (iabn_forward_train / iabn_backward, which use the channel-resident
+kernels when every channel gets its own block) and the phase entry points
+(stats + apply, reduce + apply: the streaming kernels).
+
 Three kinds of comparison:
   forward      GPU training forward vs oracle forward on the same x.
   backward     GPU backward vs oracle backward on the same stored z (the
@@ -100,12 +105,16 @@ def oracle_forward(case: Case, inp: workloads.LayerInputs):
                                 F32(case.eps), F32(case.momentum), F32(case.slope))
 
 
+PATHS = ["entry", "phases"]
+
+
+@pytest.mark.parametrize("path", PATHS)
 @pytest.mark.parametrize("case", ALL_CASES, ids=lambda c: c.id)
-def test_forward_parity(case):
+def test_forward_parity(case, path):
     inp = make_inputs(case)
-    say("forward %s shape=%s" % (case.id, (case.N, case.C, case.HW)))
+    say("forward %s %s shape=%s" % (case.id, path, (case.N, case.C, case.HW)))
     L = GpuLayer(inp)
-    L.forward_train(case.eps, case.momentum, case.slope)
+    L.forward_train(case.eps, case.momentum, case.slope, path=path)
     torch.cuda.synchronize()
     ref = oracle_forward(case, inp)
     assert_close("z", to_f64(L.x).reshape(ref["z"].shape), ref["z"], case.dtype)
@@ -116,16 +125,17 @@ def test_forward_parity(case):
         assert max_rel(got, ref[k]) <= TOL["f32"], k
 
 
+@pytest.mark.parametrize("path", PATHS)
 @pytest.mark.parametrize("case", ALL_CASES, ids=lambda c: c.id)
-def test_backward_parity(case):
+def test_backward_parity(case, path):
     inp = make_inputs(case)
     fw = oracle_forward(case, inp)
     z_store = workloads.f64_to_storage(fw["z"], case.dtype)
     var32 = fw["var"].astype(np.float32)
-    say("backward %s shape=%s" % (case.id, (case.N, case.C, case.HW)))
+    say("backward %s %s shape=%s" % (case.id, path, (case.N, case.C, case.HW)))
     L = GpuLayer(inp)
     z_dev = to_device(z_store, case.dtype)
-    L.backward(case.eps, case.slope, z=z_dev, save_var=torch.from_numpy(var32).cuda())
+    L.backward(case.eps, case.slope, z=z_dev, save_var=torch.from_numpy(var32).cuda(), path=path)
     torch.cuda.synchronize()
     ref = oracle.backward_i(workloads.storage_to_f64(z_store, case.dtype),
                             workloads.storage_to_f64(inp.dz, case.dtype), inp.gamma, inp.beta,
@@ -137,14 +147,15 @@ def test_backward_parity(case):
     assert torch.equal(z_dev, to_device(z_store, case.dtype))
 
 
+@pytest.mark.parametrize("path", PATHS)
 @pytest.mark.parametrize("case", ALL_CASES, ids=lambda c: c.id)
-def test_chain_parity(case):
+def test_chain_parity(case, path):
     """GPU forward then GPU backward, in place, against the oracle's chain."""
     inp = make_inputs(case)
-    say("chain %s shape=%s" % (case.id, (case.N, case.C, case.HW)))
+    say("chain %s %s shape=%s" % (case.id, path, (case.N, case.C, case.HW)))
     L = GpuLayer(inp)
-    L.forward_train(case.eps, case.momentum, case.slope)
-    L.backward(case.eps, case.slope)
+    L.forward_train(case.eps, case.momentum, case.slope, path=path)
+    L.backward(case.eps, case.slope, path=path)
     torch.cuda.synchronize()
     fw = oracle_forward(case, inp)
     dz = workloads.storage_to_f64(inp.dz, case.dtype)
@@ -241,17 +252,19 @@ def test_eval_parity(case):
     assert_close("z", to_f64(x).reshape(ref.shape), ref, case.dtype)
 
 
-@pytest.mark.parametrize("case", [CONFIG_CASES[3], EDGE_CASES[0], EDGE_CASES[7]], ids=lambda c: c.id)
-def test_deterministic(case):
+@pytest.mark.parametrize("path", PATHS)
+@pytest.mark.parametrize("case", [CONFIG_CASES[3], CONFIG_CASES[1], EDGE_CASES[0], EDGE_CASES[7]],
+                         ids=lambda c: c.id)
+def test_deterministic(case, path):
     """Same inputs, same device: bit-identical outputs."""
     inp = make_inputs(case)
     outs = []
     for rep in range(2):
-        say("determinism %s rep %d" % (case.id, rep))
+        say("determinism %s %s rep %d" % (case.id, path, rep))
         L = GpuLayer(inp)
-        L.forward_train(case.eps, case.momentum, case.slope)
+        L.forward_train(case.eps, case.momentum, case.slope, path=path)
         z = L.x.clone()
-        L.backward(case.eps, case.slope)
+        L.backward(case.eps, case.slope, path=path)
         torch.cuda.synchronize()
         outs.append([z, L.dz, L.save_mean, L.save_var, L.running_mean, L.running_var, L.dgamma,
                      L.dbeta])
@@ -259,21 +272,18 @@ def test_deterministic(case):
         assert torch.equal(a, b)
 
 
-@pytest.mark.parametrize("case", [CONFIG_CASES[2], EDGE_CASES[0], EDGE_CASES[7]], ids=lambda c: c.id)
-def test_phases_equal_fused(case):
-    """stats+apply and reduce+apply are exactly the fused entry points."""
+@pytest.mark.parametrize("case", [EDGE_CASES[0], EDGE_CASES[7], EDGE_CASES[3]], ids=lambda c: c.id)
+def test_phases_equal_entry_on_streaming_shapes(case):
+    """Where the entry points take the streaming kernels (few channels, or
+    the one-element path), stats+apply and reduce+apply are exactly them."""
     inp = make_inputs(case)
     say("phases %s" % case.id)
     A = GpuLayer(inp)
     A.forward_train(case.eps, case.momentum, case.slope)
     A.backward(case.eps, case.slope)
     B = GpuLayer(inp)
-    iabn.iabn_forward_stats(B.x, B.workspace)
-    iabn.iabn_forward_apply(B.x, B.gamma, B.beta, B.running_mean, B.running_var, B.save_mean,
-                            B.save_var, case.eps, case.momentum, case.slope, B.workspace)
-    iabn.iabn_backward_reduce(B.x, B.dz, B.gamma, B.beta, case.slope, B.workspace)
-    iabn.iabn_backward_apply(B.x, B.dz, B.gamma, B.beta, B.save_var, B.dgamma, B.dbeta, case.eps,
-                             case.slope, B.workspace)
+    B.forward_train(case.eps, case.momentum, case.slope, path="phases")
+    B.backward(case.eps, case.slope, path="phases")
     torch.cuda.synchronize()
     for k in ("x", "dz", "save_mean", "save_var", "running_mean", "running_var", "dgamma", "dbeta"):
         assert torch.equal(getattr(A, k), getattr(B, k)), k
@@ -344,8 +354,9 @@ def test_errors_leave_outputs_untouched():
 BACKBONE_GROUPS = [0, 3, 7, 30]  # first layer of each (C, H=W) group of the backbone sweep
 
 
+@pytest.mark.parametrize("path", PATHS)
 @pytest.mark.parametrize("layer", BACKBONE_GROUPS)
-def test_backbone_layer_sampled(layer):
+def test_backbone_layer_sampled(layer, path):
     """A full-size layer of the backbone sweep (fp16, N=8) through the same
     entry points the benchmark times; the oracle checks sampled channels,
     each computed on its own (channels are independent)."""
@@ -354,10 +365,10 @@ def test_backbone_layer_sampled(layer):
     inp = workloads.workload_layer(w, layer)
     rng = np.random.default_rng(layer)
     chans = np.unique(np.concatenate([[0, C - 1], rng.choice(C, 6, replace=False)]))
-    say("backbone layer %d shape=%s channels=%s" % (layer, (N, C, HW), chans.tolist()))
+    say("backbone layer %d %s shape=%s channels=%s" % (layer, path, (N, C, HW), chans.tolist()))
     L = GpuLayer(inp)
-    L.forward_train(w.eps, w.momentum, w.slope)
-    L.backward(w.eps, w.slope)
+    L.forward_train(w.eps, w.momentum, w.slope, path=path)
+    L.backward(w.eps, w.slope, path=path)
     torch.cuda.synchronize()
     zc = to_f64(L.x[:, chans])
     dxc = to_f64(L.dz[:, chans])
