@@ -57,6 +57,8 @@ def parse():
                     help="time budget of the oracle baseline (0 disables it)")
     ap.add_argument("--no-kernel-pass", action="store_true",
                     help="skip the per-kernel event pass (no roofline object)")
+    ap.add_argument("--phase-kernels", action="store_true",
+                    help="also time the phase entry points (the streaming kernels)")
     return ap.parse_args()
 
 
@@ -186,54 +188,63 @@ def measure(lib, args):
         % (args.steps, ms_per_step, ev_ms_per_step, value, finite))
 
     # ---------------------------------------------------------------- per-kernel pass
+    # The step's two entry points timed one by one with HIP events on the
+    # stream they run on.  On this workload each entry point is a single
+    # kernel (the channel-resident forward / backward); its algorithmic bytes
+    # are what the operation must move at least once: forward reads x and
+    # writes z (2 E b), backward reads z and dz and writes dx (3 E b).
     roofline = None
     kernels = None
-    if not args.no_kernel_pass:
+    phase_kernels = None
+
+    def timed_pass(calls):
+        """calls: list of (name, fn, args, bytes_per_elem) per layer in step order."""
+        tot_ms, tot_bytes, launches = {}, {}, {}
         refresh()
         torch.cuda.synchronize()
-        names = ("fwd_stats", "fwd_apply", "bwd_reduce", "bwd_apply")
-        tot_ms = dict.fromkeys(names, 0.0)
-        tot_bytes = dict.fromkeys(names, 0)
-        launches = dict.fromkeys(names, 0)
         for _ in range(args.steps):
             evs = []
-            for L in layers:
-                e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
-                e[0].record(stream)
-                check(lib.iabn_forward_stats(*L.stats), "iabn_forward_stats")
-                e[1].record(stream)
-                check(lib.iabn_forward_apply(*L.fwd), "iabn_forward_apply")
-                e[2].record(stream)
-                evs.append(("fwd", L, e))
-            for L in reversed(layers):
-                e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
-                e[0].record(stream)
-                check(lib.iabn_backward_reduce(*L.reduce), "iabn_backward_reduce")
-                e[1].record(stream)
-                check(lib.iabn_backward_apply(*L.bwd), "iabn_backward_apply")
-                e[2].record(stream)
-                evs.append(("bwd", L, e))
+            for name, fn, cargs, bpe, E in calls:
+                e0 = torch.cuda.Event(enable_timing=True)
+                e1 = torch.cuda.Event(enable_timing=True)
+                e0.record(stream)
+                check(fn(*cargs), name)
+                e1.record(stream)
+                evs.append((name, e0, e1, bpe * E * b))
             torch.cuda.synchronize()
-            for kind, L, e in evs:
-                first, second = ("fwd_stats", "fwd_apply") if kind == "fwd" else ("bwd_reduce",
-                                                                                  "bwd_apply")
-                for name, (a, z) in ((first, (e[0], e[1])), (second, (e[1], e[2]))):
-                    tot_ms[name] += a.elapsed_time(z)
-                    tot_bytes[name] += KERNEL_BYTES_PER_ELEM[name] * L.E * b
-                    launches[name] += 1
-        kernels = {}
-        for name in names:
-            avg_ms = tot_ms[name] / launches[name]
-            gbps = tot_bytes[name] / (tot_ms[name] * 1e-3) / 1e9
-            kernels[name] = {"avg_us": round(avg_ms * 1e3, 3), "launches": launches[name],
-                             "alg_bytes_per_launch": tot_bytes[name] // launches[name],
-                             "achieved_gbps": round(gbps, 1)}
-        dom = max(names, key=lambda n: tot_ms[n])
+            for name, e0, e1, nbytes in evs:
+                tot_ms[name] = tot_ms.get(name, 0.0) + e0.elapsed_time(e1)
+                tot_bytes[name] = tot_bytes.get(name, 0) + nbytes
+                launches[name] = launches.get(name, 0) + 1
+        out = {}
+        for name in tot_ms:
+            out[name] = {"avg_us": round(tot_ms[name] / launches[name] * 1e3, 3),
+                         "launches": launches[name],
+                         "alg_bytes_per_launch": tot_bytes[name] // launches[name],
+                         "achieved_gbps": round(tot_bytes[name] / (tot_ms[name] * 1e-3) / 1e9, 1),
+                         "share_of_pass": tot_ms[name]}
+        total = sum(tot_ms.values())
+        for name in out:
+            out[name]["share_of_pass"] = round(out[name]["share_of_pass"] / total, 4)
+        return out
+
+    if not args.no_kernel_pass:
+        entry = ([("iabn_forward_train", fwd_train, L.fwd, 2, L.E) for L in layers] +
+                 [("iabn_backward", backward, L.bwd, 3, L.E) for L in reversed(layers)])
+        kernels = timed_pass(entry)
+        dom = max(kernels, key=lambda n: kernels[n]["share_of_pass"])
         k = kernels[dom]
         roofline = {"bound": "hbm", "kernel": dom, "achieved": k["achieved_gbps"],
                     "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                     "frac": round(k["achieved_gbps"] / HBM_PEAK_GBPS, 4), "traffic": None}
-        log("per-kernel: " + json.dumps(kernels))
+        log("entry points: " + json.dumps(kernels))
+    if args.phase_kernels:
+        phases = ([x for L in layers for x in (("iabn_forward_stats", lib.iabn_forward_stats, L.stats, 1, L.E),
+                                                ("iabn_forward_apply", lib.iabn_forward_apply, L.fwd, 2, L.E))] +
+                  [x for L in reversed(layers) for x in (("iabn_backward_reduce", lib.iabn_backward_reduce, L.reduce, 2, L.E),
+                                                          ("iabn_backward_apply", lib.iabn_backward_apply, L.bwd, 3, L.E))])
+        phase_kernels = timed_pass(phases)
+        log("phase entry points: " + json.dumps(phase_kernels))
 
     # ---------------------------------------------------------------- CPU baseline
     cpu = None
@@ -290,6 +301,8 @@ def measure(lib, args):
         "config": {"workload": w.name, "storage": w.dtype, "layers": len(w.layers),
                    "elements_per_tensor": E_total, "slope": w.slope, "eps": w.eps,
                    "momentum": w.momentum},
+        # floor: every tensor crosses HBM once (x in, z out, z and dz in, dx
+        # out); schedule: the two-pass streaming schedule (x, z, dz read twice).
         "hbm": {"schedule_bytes_per_step": sched_bytes,
                 "schedule_gbps": round(sched_bytes / (ms_per_step * 1e-3) / 1e9, 1),
                 "schedule_frac_of_peak": round(sched_bytes / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
@@ -300,6 +313,7 @@ def measure(lib, args):
         "activation_memory": {"iabn_stored_bytes": E_total * b,
                               "store_x_baseline_bytes": 2 * E_total * b},
         "kernels": kernels,
+        "phase_kernels": phase_kernels,
         "roofline": roofline,
         "cpu_baseline": cpu,
     }

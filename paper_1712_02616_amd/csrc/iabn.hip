@@ -585,6 +585,11 @@ __device__ __forceinline__ void opaque(V& v) {
     asm volatile("" : "+v"(v));
 }
 
+// Keep the scheduler from interleaving the per-access steps of the register-
+// resident loops: interleaving them only raises register pressure (the loads
+// are already all in flight), and past the block's register budget it spills.
+__device__ __forceinline__ void sched_fence() { __builtin_amdgcn_sched_barrier(0); }
+
 template <int HINT>
 __device__ __forceinline__ raw16_t load_raw(const void* __restrict__ base, uint64_t idx) {
     const raw16_t* p = static_cast<const raw16_t*>(base) + idx;
@@ -674,20 +679,66 @@ __device__ __forceinline__ void block_sums(double a, double b, double& sa, doubl
     sb = out[1];
 }
 
+// Where each row of a channel holds a whole number of T-wide strips of
+// 16-byte accesses (vrow % T == 0) and the channel has at least R strips,
+// access k of every thread of the block lies in strip k: its index is a
+// block-uniform strip offset plus the thread index, and every thread has an
+// access in each of the vchan / T strips.  The strip offsets are scalar
+// (SGPR) arithmetic and the R resident accesses need no bounds test, so the
+// per-element path spends no vector instructions on addresses or bounds.
+// STRIP = false is the general mapping (row division per access, bounds per
+// lane).
+struct StripPos {
+    uint64_t off;  // index of the strip's first access
+    uint32_t col;  // column of the strip within its row
+};
+
+__device__ __forceinline__ StripPos strip_begin(const Geom& g, uint32_t c) {
+    StripPos s;
+    s.off = static_cast<uint64_t>(c) * g.vrow;
+    s.col = 0;
+    return s;
+}
+
+template <int T>
+__device__ __forceinline__ void strip_next(const Geom& g, StripPos& s) {
+    s.col += T;
+    s.off += T;
+    if (s.col == g.vrow) {
+        s.col = 0;
+        s.off += g.nstride - g.vrow;
+    }
+}
+
+// The leaky ReLU as max(y, a*y) for a <= 1 and min(y, a*y) for a > 1: two
+// instructions, and the same value as the definition's branch (including
+// y = -0, which stays -0).
+template <bool SMALL_SLOPE>
+__device__ __forceinline__ float leaky(float y, float a) {
+    return SMALL_SLOPE ? fmaxf(y, a * y) : fminf(y, a * y);
+}
+
 // Training forward of one channel per block (statistics, running estimates,
 // z over x), same arithmetic as fwd_stats_kernel + fwd_apply_kernel.
-template <int DT, int VEC, int T, int R>
-__global__ __launch_bounds__(T) void fwd_fused_kernel(void* __restrict__ xz, Geom g,
-                                                      FwdParams prm) {
-    const uint32_t c = blockIdx.x;
+template <int DT, int VEC, int T, int R, bool STRIP>
+__device__ __forceinline__ void fwd_fused_channel(void* __restrict__ xz, const Geom& g,
+                                                  const FwdParams& prm, uint32_t c) {
     const uint64_t cbase = static_cast<uint64_t>(c) * g.vrow;
     const uint32_t tid = threadIdx.x;
+    const uint32_t nstrips = STRIP ? g.vchan / T : 0;
+    raw16_t* const xv = static_cast<raw16_t*>(xz);
 
     raw16_t keep[R];
+    StripPos sp = strip_begin(g, c);
 #pragma unroll
     for (int k = 0; k < R; ++k) {
-        const uint32_t v = tid + k * T;
-        if (v < g.vchan) keep[k] = load_raw<kCached>(xz, access_index(g, cbase, v));
+        if constexpr (STRIP) {
+            keep[k] = (xv + sp.off)[tid];
+            strip_next<T>(g, sp);
+        } else {
+            const uint32_t v = tid + k * T;
+            if (v < g.vchan) keep[k] = load_raw<kCached>(xz, access_index(g, cbase, v));
+        }
     }
     float shift = 0.f, s1 = 0.f, s2 = 0.f;
     uint32_t nacc = 0;
@@ -696,25 +747,9 @@ __global__ __launch_bounds__(T) void fwd_fused_kernel(void* __restrict__ xz, Geo
         unpack<DT, VEC>(keep[0], t);
         shift = t[0];
     }
-#pragma unroll
-    for (int k = 0; k < R; ++k) {
-        const uint32_t v = tid + k * T;
-        if (v < g.vchan) {
-            float t[VEC];
-            unpack<DT, VEC>(keep[k], t);
-#pragma unroll
-            for (int e = 0; e < VEC; ++e) {
-                const float d = t[e] - shift;
-                s1 += d;
-                s2 = fmaf(d, d, s2);
-            }
-            ++nacc;
-        }
-    }
-#pragma unroll 1
-    for (uint32_t v = tid + R * T; v < g.vchan; v += T) {
+    auto accumulate = [&](raw16_t r) {
         float t[VEC];
-        unpack<DT, VEC>(load_raw<kCached>(xz, access_index(g, cbase, v)), t);
+        unpack<DT, VEC>(r, t);
 #pragma unroll
         for (int e = 0; e < VEC; ++e) {
             const float d = t[e] - shift;
@@ -722,6 +757,22 @@ __global__ __launch_bounds__(T) void fwd_fused_kernel(void* __restrict__ xz, Geo
             s2 = fmaf(d, d, s2);
         }
         ++nacc;
+    };
+#pragma unroll
+    for (int k = 0; k < R; ++k) {
+        if (STRIP || tid + k * T < g.vchan) accumulate(keep[k]);
+        sched_fence();
+    }
+    if constexpr (STRIP) {
+#pragma unroll 1
+        for (uint32_t k = R; k < nstrips; ++k) {
+            accumulate((xv + sp.off)[tid]);
+            strip_next<T>(g, sp);
+        }
+    } else {
+#pragma unroll 1
+        for (uint32_t v = tid + R * T; v < g.vchan; v += T)
+            accumulate(load_raw<kCached>(xz, access_index(g, cbase, v)));
     }
 
     double mean, var;
@@ -730,11 +781,12 @@ __global__ __launch_bounds__(T) void fwd_fused_kernel(void* __restrict__ xz, Geo
     opaque(tid2);
 #pragma unroll
     for (int k = 0; k < R; ++k) opaque(keep[k]);
+    const double scale_d = static_cast<double>(prm.gamma[c]) / sqrt(var + static_cast<double>(prm.eps));
     const float mean_hi = static_cast<float>(mean);
-    const float mean_lo = static_cast<float>(mean - static_cast<double>(mean_hi));
-    const float scale = static_cast<float>(static_cast<double>(prm.gamma[c]) /
-                                           sqrt(var + static_cast<double>(prm.eps)));
-    const float bshift = prm.beta[c];
+    const double mean_lo = mean - static_cast<double>(mean_hi);
+    const float scale = static_cast<float>(scale_d);
+    // (x - mu) * scale + beta with mu = mean_hi + mean_lo: the low part goes into the shift.
+    const float bshift = static_cast<float>(static_cast<double>(prm.beta[c]) - mean_lo * scale_d);
     const float slope = prm.slope;
     if (tid == 0) {
         const double mom = prm.momentum;
@@ -746,83 +798,81 @@ __global__ __launch_bounds__(T) void fwd_fused_kernel(void* __restrict__ xz, Geo
         prm.running_var[c] = static_cast<float>(
             (1.0 - mom) * static_cast<double>(prm.running_var[c]) + mom * var * (m / (m - 1.0)));
     }
-    auto act = [&](float xv) {
-        const float y = fmaf((xv - mean_hi) - mean_lo, scale, bshift);
-        return y >= 0.f ? y : slope * y;
-    };
 
-#pragma unroll
-    for (int k = 0; k < R; ++k) {
-        const uint32_t v = tid2 + k * T;
-        if (v < g.vchan) {
+    auto apply_all = [&](auto act) {
+        auto emit = [&](raw16_t r, uint64_t idx) {
             float t[VEC];
-            unpack<DT, VEC>(keep[k], t);
+            unpack<DT, VEC>(r, t);
 #pragma unroll
-            for (int e = 0; e < VEC; ++e) t[e] = act(t[e]);
-            store_vec<DT, VEC, kHintFwdApplyStore>(xz, access_index(g, cbase, v), t);
+            for (int e = 0; e < VEC; ++e) t[e] = act(fmaf(t[e] - mean_hi, scale, bshift));
+            store_vec<DT, VEC, kHintFwdApplyStore>(xz, idx, t);
+        };
+        StripPos sq = strip_begin(g, c);
+#pragma unroll
+        for (int k = 0; k < R; ++k) {
+            if constexpr (STRIP) {
+                emit(keep[k], sq.off + tid2);
+                strip_next<T>(g, sq);
+            } else {
+                const uint32_t v = tid2 + k * T;
+                if (v < g.vchan) emit(keep[k], access_index(g, cbase, v));
+            }
+            sched_fence();
         }
-    }
+        if constexpr (STRIP) {
 #pragma unroll 1
-    for (uint32_t v = tid2 + R * T; v < g.vchan; v += T) {
-        float t[VEC];
-        const uint64_t i1 = access_index(g, cbase, v);
-        unpack<DT, VEC>(load_raw<kStream>(xz, i1), t);
-#pragma unroll
-        for (int e = 0; e < VEC; ++e) t[e] = act(t[e]);
-        store_vec<DT, VEC, kHintFwdApplyStore>(xz, i1, t);
-    }
+            for (uint32_t k = R; k < nstrips; ++k) {
+                emit(load_raw<kStream>(xz, sq.off + tid2), sq.off + tid2);
+                strip_next<T>(g, sq);
+            }
+        } else {
+#pragma unroll 1
+            for (uint32_t v = tid2 + R * T; v < g.vchan; v += T) {
+                const uint64_t i1 = access_index(g, cbase, v);
+                emit(load_raw<kStream>(xz, i1), i1);
+            }
+        }
+    };
+    if (slope <= 1.f) apply_all([&](float y) { return leaky<true>(y, slope); });
+    else apply_all([&](float y) { return leaky<false>(y, slope); });
 }
 
 // Backward of one channel per block (sums of dy and dy*xhat, dgamma, dbeta,
 // dx over dz), same arithmetic as bwd_reduce_kernel + bwd_apply_kernel.
-template <int DT, int VEC, int T, int R>
-__global__ __launch_bounds__(T) void bwd_fused_kernel(const void* __restrict__ z,
-                                                      void* __restrict__ dzdx, Geom g,
-                                                      BwdParams prm) {
-    const uint32_t c = blockIdx.x;
+template <int DT, int VEC, int T, int R, bool STRIP>
+__device__ __forceinline__ void bwd_fused_channel(const void* __restrict__ z,
+                                                  void* __restrict__ dzdx, const Geom& g,
+                                                  const BwdParams& prm, uint32_t c) {
     const uint64_t cbase = static_cast<uint64_t>(c) * g.vrow;
     const uint32_t tid = threadIdx.x;
+    const uint32_t nstrips = STRIP ? g.vchan / T : 0;
+    const raw16_t* const zv = static_cast<const raw16_t*>(z);
+    const raw16_t* const gv = static_cast<const raw16_t*>(dzdx);
     const BwdElem el = {prm.slope, 1.0f / prm.slope, prm.beta[c], 1.0f / prm.gamma[c]};
 
     raw16_t kz[R], kg[R];
+    StripPos sp = strip_begin(g, c);
 #pragma unroll
     for (int k = 0; k < R; ++k) {
-        const uint32_t v = tid + k * T;
-        if (v < g.vchan) {
-            const uint64_t i1 = access_index(g, cbase, v);
-            kz[k] = load_raw<kCached>(z, i1);
-            kg[k] = load_raw<kCached>(dzdx, i1);
+        if constexpr (STRIP) {
+            kz[k] = (zv + sp.off)[tid];
+            kg[k] = (gv + sp.off)[tid];
+            strip_next<T>(g, sp);
+        } else {
+            const uint32_t v = tid + k * T;
+            if (v < g.vchan) {
+                const uint64_t i1 = access_index(g, cbase, v);
+                kz[k] = load_raw<kCached>(z, i1);
+                kg[k] = load_raw<kCached>(dzdx, i1);
+            }
         }
     }
     double acc_dy = 0.0, acc_dyx = 0.0;
-    {
-        float sdy = 0.f, sdyx = 0.f;
-#pragma unroll
-        for (int k = 0; k < R; ++k) {
-            const uint32_t v = tid + k * T;
-            if (v < g.vchan) {
-                float tz[VEC], tg[VEC];
-                unpack<DT, VEC>(kz[k], tz);
-                unpack<DT, VEC>(kg[k], tg);
-#pragma unroll
-                for (int e = 0; e < VEC; ++e) {
-                    float dy, xhat;
-                    el(tz[e], tg[e], dy, xhat);
-                    sdy += dy;
-                    sdyx = fmaf(dy, xhat, sdyx);
-                }
-            }
-        }
-        acc_dy = sdy;
-        acc_dyx = sdyx;
-    }
-#pragma unroll 1
-    for (uint32_t v = tid + R * T; v < g.vchan; v += T) {
+    float sdy = 0.f, sdyx = 0.f;
+    auto accumulate = [&](raw16_t rz, raw16_t rg) {
         float tz[VEC], tg[VEC];
-        const uint64_t i1 = access_index(g, cbase, v);
-        unpack<DT, VEC>(load_raw<kCached>(z, i1), tz);
-        unpack<DT, VEC>(load_raw<kCached>(dzdx, i1), tg);
-        float sdy = 0.f, sdyx = 0.f;
+        unpack<DT, VEC>(rz, tz);
+        unpack<DT, VEC>(rg, tg);
 #pragma unroll
         for (int e = 0; e < VEC; ++e) {
             float dy, xhat;
@@ -830,8 +880,34 @@ __global__ __launch_bounds__(T) void bwd_fused_kernel(const void* __restrict__ z
             sdy += dy;
             sdyx = fmaf(dy, xhat, sdyx);
         }
-        acc_dy += sdy;
-        acc_dyx += sdyx;
+    };
+#pragma unroll
+    for (int k = 0; k < R; ++k) {
+        if (STRIP || tid + k * T < g.vchan) accumulate(kz[k], kg[k]);
+        sched_fence();
+    }
+    acc_dy = sdy;
+    acc_dyx = sdyx;
+    if constexpr (STRIP) {
+#pragma unroll 1
+        for (uint32_t k = R; k < nstrips; ++k) {
+            sdy = 0.f;
+            sdyx = 0.f;
+            accumulate((zv + sp.off)[tid], (gv + sp.off)[tid]);
+            acc_dy += sdy;
+            acc_dyx += sdyx;
+            strip_next<T>(g, sp);
+        }
+    } else {
+#pragma unroll 1
+        for (uint32_t v = tid + R * T; v < g.vchan; v += T) {
+            const uint64_t i1 = access_index(g, cbase, v);
+            sdy = 0.f;
+            sdyx = 0.f;
+            accumulate(load_raw<kCached>(z, i1), load_raw<kCached>(dzdx, i1));
+            acc_dy += sdy;
+            acc_dyx += sdyx;
+        }
     }
 
     double dbeta, dgamma;
@@ -853,34 +929,61 @@ __global__ __launch_bounds__(T) void bwd_fused_kernel(const void* __restrict__ z
         prm.dgamma[c] = static_cast<float>(dgamma);
         prm.dbeta[c] = static_cast<float>(dbeta);
     }
-    auto dx_of = [&](float zv, float gv) {
-        float dy, xhat;
-        el(zv, gv, dy, xhat);
-        return fmaf(ca, dy, fmaf(cb, xhat, cc));
+    auto emit = [&](raw16_t rz, raw16_t rg, uint64_t idx) {
+        float tz[VEC], tg[VEC];
+        unpack<DT, VEC>(rz, tz);
+        unpack<DT, VEC>(rg, tg);
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) {
+            float dy, xhat;
+            el(tz[e], tg[e], dy, xhat);
+            tg[e] = fmaf(ca, dy, fmaf(cb, xhat, cc));
+        }
+        store_vec<DT, VEC, kHintBwdApplyStore>(dzdx, idx, tg);
     };
-
+    StripPos sq = strip_begin(g, c);
 #pragma unroll
     for (int k = 0; k < R; ++k) {
-        const uint32_t v = tid2 + k * T;
-        if (v < g.vchan) {
-            float tz[VEC], tg[VEC];
-            unpack<DT, VEC>(kz[k], tz);
-            unpack<DT, VEC>(kg[k], tg);
-#pragma unroll
-            for (int e = 0; e < VEC; ++e) tg[e] = dx_of(tz[e], tg[e]);
-            store_vec<DT, VEC, kHintBwdApplyStore>(dzdx, access_index(g, cbase, v), tg);
+        if constexpr (STRIP) {
+            emit(kz[k], kg[k], sq.off + tid2);
+            strip_next<T>(g, sq);
+        } else {
+            const uint32_t v = tid2 + k * T;
+            if (v < g.vchan) emit(kz[k], kg[k], access_index(g, cbase, v));
+        }
+        sched_fence();
+    }
+    if constexpr (STRIP) {
+#pragma unroll 1
+        for (uint32_t k = R; k < nstrips; ++k) {
+            const uint64_t i1 = sq.off + tid2;
+            emit(load_raw<kStream>(z, i1), load_raw<kStream>(dzdx, i1), i1);
+            strip_next<T>(g, sq);
+        }
+    } else {
+#pragma unroll 1
+        for (uint32_t v = tid2 + R * T; v < g.vchan; v += T) {
+            const uint64_t i1 = access_index(g, cbase, v);
+            emit(load_raw<kStream>(z, i1), load_raw<kStream>(dzdx, i1), i1);
         }
     }
-#pragma unroll 1
-    for (uint32_t v = tid2 + R * T; v < g.vchan; v += T) {
-        float tz[VEC], tg[VEC];
-        const uint64_t i1 = access_index(g, cbase, v);
-        unpack<DT, VEC>(load_raw<kStream>(z, i1), tz);
-        unpack<DT, VEC>(load_raw<kStream>(dzdx, i1), tg);
-#pragma unroll
-        for (int e = 0; e < VEC; ++e) tg[e] = dx_of(tz[e], tg[e]);
-        store_vec<DT, VEC, kHintBwdApplyStore>(dzdx, i1, tg);
-    }
+}
+
+// One block per channel: c = blockIdx.x.  (Looping a block over several
+// channels was measured slower: the loop made the compiler keep more values
+// live and halved occupancy, and overlapping one channel's stores with the
+// next one's loads gained nothing over the hardware's own block scheduling.)
+template <int DT, int VEC, int T, int R, bool STRIP>
+__global__ __launch_bounds__(T) void fwd_fused_kernel(void* __restrict__ xz, Geom g,
+                                                      FwdParams prm) {
+    fwd_fused_channel<DT, VEC, T, R, STRIP>(xz, g, prm, blockIdx.x);
+}
+
+template <int DT, int VEC, int T, int R, bool STRIP>
+__global__ __launch_bounds__(T) void bwd_fused_kernel(const void* __restrict__ z,
+                                                      void* __restrict__ dzdx, Geom g,
+                                                      BwdParams prm) {
+    bwd_fused_channel<DT, VEC, T, R, STRIP>(z, dzdx, g, prm, blockIdx.x);
 }
 
 // ---------------------------------------------------------------- host side
@@ -1080,46 +1183,89 @@ struct FusedPlan {
     int R;  // 16-byte accesses per thread held in registers (per tensor)
 };
 
-// The first of (T, R) = (256, 4), (512, 4), (256, 16), (512, 16) whose
-// threads hold the whole channel; larger channels take 1024 threads with
-// R = 16 (forward) or 8 (backward, two tensors) and re-read the remainder.
+dim3 fused_grid(const Geom& g, const FusedPlan&) { return dim3(g.C); }
+
+// Resident blocks per CU of a fused launch (0: as many as registers allow).
+// Fewer resident blocks run the channels in several rounds, so the loads of
+// a later round overlap the stores of an earlier one instead of every block
+// reading, then every block writing.  The cap is applied by reserving LDS.
+constexpr int kFusedFwdBlocksPerCU = 0;
+constexpr int kFusedBwdBlocksPerCU = 0;
+constexpr size_t kLdsPerCU = 160 * 1024;
+
+size_t fused_lds(int blocks_per_cu) {
+    if (blocks_per_cu <= 0) return 0;
+    return kLdsPerCU / blocks_per_cu - 2048;  // leaves room for the kernels' own reduction buffers
+}
+
+// Candidate (T, R) in order of preference: the first whose threads hold the
+// whole channel is used; larger channels take the last entry and re-read
+// the remainder.  The backward holds two tensors, so its largest blocks keep
+// half as many accesses per thread.
+// Fused kernels use strip addressing where the shape allows it.
+constexpr bool kUseStrips = true;
+
+constexpr FusedPlan kFwdLadder[] = {{256, 4}, {512, 4}, {256, 16}, {512, 16}, {1024, 16}};
+constexpr FusedPlan kBwdLadder[] = {{256, 4}, {512, 4}, {256, 16}, {512, 16}, {1024, 8}};
+
 bool plan_fused(int64_t C, const Geom& g, bool vector, bool backward, FusedPlan* out) {
     if (!vector || C < kFusedMinChannels) return false;
     const int64_t A = g.vchan;
-    const FusedPlan ladder[4] = {{256, 4}, {512, 4}, {256, 16}, {512, 16}};
-    for (const FusedPlan& fp : ladder) {
-        if (A <= static_cast<int64_t>(fp.T) * fp.R) {
-            *out = fp;
+    const FusedPlan* ladder = backward ? kBwdLadder : kFwdLadder;
+    const int n = backward ? int(sizeof kBwdLadder / sizeof kBwdLadder[0])
+                           : int(sizeof kFwdLadder / sizeof kFwdLadder[0]);
+    for (int i = 0; i < n; ++i) {
+        if (A <= static_cast<int64_t>(ladder[i].T) * ladder[i].R || i == n - 1) {
+            *out = ladder[i];
             return true;
         }
     }
-    *out = {1024, backward ? 8 : 16};
-    return true;
+    return false;
 }
 
+#define IABN_FUSED_CASE(KERNEL, TT, RR, ...)                                                   \
+    if (fp.T == TT && fp.R == RR) {                                                           \
+        if (kUseStrips && g.vrow % TT == 0 && g.vchan / TT >= RR)                             \
+            KERNEL<DT, V, TT, RR, true><<<grid, TT, lds, st>>>(__VA_ARGS__);                  \
+        else                                                                                  \
+            KERNEL<DT, V, TT, RR, false><<<grid, TT, lds, st>>>(__VA_ARGS__);                 \
+        return true;                                                                          \
+    }
+
 template <int DT>
-void launch_fwd_fused(void* xz, const Geom& g, const FusedPlan& fp, const FwdParams& prm,
+bool launch_fwd_fused(void* xz, const Geom& g, const FusedPlan& fp, const FwdParams& prm,
                       hipStream_t st) {
     constexpr int V = 16 / sizeof(typename Elem<DT>::T);
-    const dim3 grid(g.C);
-    if (fp.T == 256 && fp.R == 4) fwd_fused_kernel<DT, V, 256, 4><<<grid, 256, 0, st>>>(xz, g, prm);
-    else if (fp.T == 512 && fp.R == 4) fwd_fused_kernel<DT, V, 512, 4><<<grid, 512, 0, st>>>(xz, g, prm);
-    else if (fp.T == 256) fwd_fused_kernel<DT, V, 256, 16><<<grid, 256, 0, st>>>(xz, g, prm);
-    else if (fp.T == 512) fwd_fused_kernel<DT, V, 512, 16><<<grid, 512, 0, st>>>(xz, g, prm);
-    else fwd_fused_kernel<DT, V, 1024, 16><<<grid, 1024, 0, st>>>(xz, g, prm);
+    const dim3 grid = fused_grid(g, fp);
+    const size_t lds = fused_lds(kFusedFwdBlocksPerCU);
+    IABN_FUSED_CASE(fwd_fused_kernel, 256, 4, xz, g, prm)
+    IABN_FUSED_CASE(fwd_fused_kernel, 512, 4, xz, g, prm)
+    IABN_FUSED_CASE(fwd_fused_kernel, 1024, 4, xz, g, prm)
+    IABN_FUSED_CASE(fwd_fused_kernel, 256, 16, xz, g, prm)
+    IABN_FUSED_CASE(fwd_fused_kernel, 512, 8, xz, g, prm)
+    IABN_FUSED_CASE(fwd_fused_kernel, 512, 16, xz, g, prm)
+    IABN_FUSED_CASE(fwd_fused_kernel, 1024, 8, xz, g, prm)
+    IABN_FUSED_CASE(fwd_fused_kernel, 1024, 16, xz, g, prm)
+    return false;
 }
 
 template <int DT>
-void launch_bwd_fused(const void* z, void* dzdx, const Geom& g, const FusedPlan& fp,
+bool launch_bwd_fused(const void* z, void* dzdx, const Geom& g, const FusedPlan& fp,
                       const BwdParams& prm, hipStream_t st) {
     constexpr int V = 16 / sizeof(typename Elem<DT>::T);
-    const dim3 grid(g.C);
-    if (fp.T == 256 && fp.R == 4) bwd_fused_kernel<DT, V, 256, 4><<<grid, 256, 0, st>>>(z, dzdx, g, prm);
-    else if (fp.T == 512 && fp.R == 4) bwd_fused_kernel<DT, V, 512, 4><<<grid, 512, 0, st>>>(z, dzdx, g, prm);
-    else if (fp.T == 256) bwd_fused_kernel<DT, V, 256, 16><<<grid, 256, 0, st>>>(z, dzdx, g, prm);
-    else if (fp.T == 512) bwd_fused_kernel<DT, V, 512, 16><<<grid, 512, 0, st>>>(z, dzdx, g, prm);
-    else bwd_fused_kernel<DT, V, 1024, 8><<<grid, 1024, 0, st>>>(z, dzdx, g, prm);
+    const dim3 grid = fused_grid(g, fp);
+    const size_t lds = fused_lds(kFusedBwdBlocksPerCU);
+    IABN_FUSED_CASE(bwd_fused_kernel, 256, 4, z, dzdx, g, prm)
+    IABN_FUSED_CASE(bwd_fused_kernel, 512, 4, z, dzdx, g, prm)
+    IABN_FUSED_CASE(bwd_fused_kernel, 1024, 4, z, dzdx, g, prm)
+    IABN_FUSED_CASE(bwd_fused_kernel, 256, 16, z, dzdx, g, prm)
+    IABN_FUSED_CASE(bwd_fused_kernel, 512, 8, z, dzdx, g, prm)
+    IABN_FUSED_CASE(bwd_fused_kernel, 512, 16, z, dzdx, g, prm)
+    IABN_FUSED_CASE(bwd_fused_kernel, 1024, 8, z, dzdx, g, prm)
+    return false;
 }
+
+#undef IABN_FUSED_CASE
 
 // ---- end fused planning
 
@@ -1218,9 +1364,10 @@ int iabn_forward_train(void* x_z, int dtype, const float* gamma, const float* be
         const FwdParams prm = {gamma, beta, running_mean, running_var, save_mean, save_var,
                                eps,   momentum, slope};
         const hipStream_t st = static_cast<hipStream_t>(stream);
-        if (dtype == IABN_F32) launch_fwd_fused<IABN_F32>(x_z, g, fp, prm, st);
-        else if (dtype == IABN_F16) launch_fwd_fused<IABN_F16>(x_z, g, fp, prm, st);
-        else launch_fwd_fused<IABN_BF16>(x_z, g, fp, prm, st);
+        const bool ok = dtype == IABN_F32   ? launch_fwd_fused<IABN_F32>(x_z, g, fp, prm, st)
+                        : dtype == IABN_F16 ? launch_fwd_fused<IABN_F16>(x_z, g, fp, prm, st)
+                                            : launch_fwd_fused<IABN_BF16>(x_z, g, fp, prm, st);
+        if (!ok) return fail(IABN_ERR_HIP, "no forward kernel built for T=%d R=%d", fp.T, fp.R);
         return launched("fwd_fused");
     }
     if ((rc = iabn_forward_stats(x_z, dtype, N, C, HW, workspace, workspace_bytes, stream)))
@@ -1302,9 +1449,10 @@ int iabn_backward(const void* z, void* dz_dx, int dtype, const float* gamma, con
     if (plan_fused(C, g, vec, true, &fp)) {
         const BwdParams prm = {gamma, beta, save_var, dgamma, dbeta, eps, slope};
         const hipStream_t st = static_cast<hipStream_t>(stream);
-        if (dtype == IABN_F32) launch_bwd_fused<IABN_F32>(z, dz_dx, g, fp, prm, st);
-        else if (dtype == IABN_F16) launch_bwd_fused<IABN_F16>(z, dz_dx, g, fp, prm, st);
-        else launch_bwd_fused<IABN_BF16>(z, dz_dx, g, fp, prm, st);
+        const bool ok = dtype == IABN_F32   ? launch_bwd_fused<IABN_F32>(z, dz_dx, g, fp, prm, st)
+                        : dtype == IABN_F16 ? launch_bwd_fused<IABN_F16>(z, dz_dx, g, fp, prm, st)
+                                            : launch_bwd_fused<IABN_BF16>(z, dz_dx, g, fp, prm, st);
+        if (!ok) return fail(IABN_ERR_HIP, "no backward kernel built for T=%d R=%d", fp.T, fp.R);
         return launched("bwd_fused");
     }
     if ((rc = iabn_backward_reduce(z, dz_dx, dtype, gamma, beta, slope, N, C, HW, workspace,
