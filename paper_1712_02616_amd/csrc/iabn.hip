@@ -710,12 +710,79 @@ __device__ __forceinline__ void strip_next(const Geom& g, StripPos& s) {
     }
 }
 
+// The same for a block-uniform strip position (kept in scalar registers):
+// the apply phase walks the strips again instead of keeping every strip
+// offset of the reduction phase alive.
+__device__ __forceinline__ void opaque_uniform(StripPos& s) {
+    asm volatile("" : "+s"(s.off), "+s"(s.col));
+}
+
 // The leaky ReLU as max(y, a*y) for a <= 1 and min(y, a*y) for a > 1: two
 // instructions, and the same value as the definition's branch (including
 // y = -0, which stays -0).
 template <bool SMALL_SLOPE>
 __device__ __forceinline__ float leaky(float y, float a) {
     return SMALL_SLOPE ? fmaxf(y, a * y) : fminf(y, a * y);
+}
+
+// Apply phase of the fused forward: z = f((x - mean_hi) * scale + bshift) for
+// the thread's resident accesses (from registers) and the remainder (loaded
+// again), stored over x.
+template <int DT, int VEC, int T, int R, bool STRIP, bool SMALL_SLOPE>
+__device__ __forceinline__ void fwd_fused_apply(void* __restrict__ xz, const Geom& g, uint32_t c,
+                                                uint32_t tid, const raw16_t (&keep)[R],
+                                                float mean_hi, float scale, float bshift,
+                                                float slope) {
+    const uint64_t cbase = static_cast<uint64_t>(c) * g.vrow;
+    const uint32_t nstrips = STRIP ? g.vchan / T : 0;
+    StripPos sq = strip_begin(g, c);
+    opaque_uniform(sq);
+#pragma unroll
+    for (int k = 0; k < R; ++k) {
+        uint64_t idx = 0;
+        bool live = true;
+        if constexpr (STRIP) {
+            idx = sq.off + tid;
+            strip_next<T>(g, sq);
+        } else {
+            const uint32_t v = tid + k * T;
+            live = v < g.vchan;
+            if (live) idx = access_index(g, cbase, v);
+        }
+        if (live) {
+            float t[VEC];
+            unpack<DT, VEC>(keep[k], t);
+#pragma unroll
+            for (int e = 0; e < VEC; ++e)
+                t[e] = leaky<SMALL_SLOPE>(fmaf(t[e] - mean_hi, scale, bshift), slope);
+            store_vec<DT, VEC, kHintFwdApplyStore>(xz, idx, t);
+        }
+        sched_fence();
+    }
+    if constexpr (STRIP) {
+#pragma unroll 1
+        for (uint32_t k = R; k < nstrips; ++k) {
+            const uint64_t idx = sq.off + tid;
+            float t[VEC];
+            unpack<DT, VEC>(load_raw<kStream>(xz, idx), t);
+#pragma unroll
+            for (int e = 0; e < VEC; ++e)
+                t[e] = leaky<SMALL_SLOPE>(fmaf(t[e] - mean_hi, scale, bshift), slope);
+            store_vec<DT, VEC, kHintFwdApplyStore>(xz, idx, t);
+            strip_next<T>(g, sq);
+        }
+    } else {
+#pragma unroll 1
+        for (uint32_t v = tid + R * T; v < g.vchan; v += T) {
+            const uint64_t idx = access_index(g, cbase, v);
+            float t[VEC];
+            unpack<DT, VEC>(load_raw<kStream>(xz, idx), t);
+#pragma unroll
+            for (int e = 0; e < VEC; ++e)
+                t[e] = leaky<SMALL_SLOPE>(fmaf(t[e] - mean_hi, scale, bshift), slope);
+            store_vec<DT, VEC, kHintFwdApplyStore>(xz, idx, t);
+        }
+    }
 }
 
 // Training forward of one channel per block (statistics, running estimates,
@@ -760,7 +827,17 @@ __device__ __forceinline__ void fwd_fused_channel(void* __restrict__ xz, const G
     };
 #pragma unroll
     for (int k = 0; k < R; ++k) {
-        if (STRIP || tid + k * T < g.vchan) accumulate(keep[k]);
+        if (STRIP || tid + k * T < g.vchan) {
+            float t[VEC];
+            unpack<DT, VEC>(keep[k], t);
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) {
+                const float d = t[e] - shift;
+                s1 += d;
+                s2 = fmaf(d, d, s2);
+            }
+            ++nacc;
+        }
         sched_fence();
     }
     if constexpr (STRIP) {
@@ -799,42 +876,10 @@ __device__ __forceinline__ void fwd_fused_channel(void* __restrict__ xz, const G
             (1.0 - mom) * static_cast<double>(prm.running_var[c]) + mom * var * (m / (m - 1.0)));
     }
 
-    auto apply_all = [&](auto act) {
-        auto emit = [&](raw16_t r, uint64_t idx) {
-            float t[VEC];
-            unpack<DT, VEC>(r, t);
-#pragma unroll
-            for (int e = 0; e < VEC; ++e) t[e] = act(fmaf(t[e] - mean_hi, scale, bshift));
-            store_vec<DT, VEC, kHintFwdApplyStore>(xz, idx, t);
-        };
-        StripPos sq = strip_begin(g, c);
-#pragma unroll
-        for (int k = 0; k < R; ++k) {
-            if constexpr (STRIP) {
-                emit(keep[k], sq.off + tid2);
-                strip_next<T>(g, sq);
-            } else {
-                const uint32_t v = tid2 + k * T;
-                if (v < g.vchan) emit(keep[k], access_index(g, cbase, v));
-            }
-            sched_fence();
-        }
-        if constexpr (STRIP) {
-#pragma unroll 1
-            for (uint32_t k = R; k < nstrips; ++k) {
-                emit(load_raw<kStream>(xz, sq.off + tid2), sq.off + tid2);
-                strip_next<T>(g, sq);
-            }
-        } else {
-#pragma unroll 1
-            for (uint32_t v = tid2 + R * T; v < g.vchan; v += T) {
-                const uint64_t i1 = access_index(g, cbase, v);
-                emit(load_raw<kStream>(xz, i1), i1);
-            }
-        }
-    };
-    if (slope <= 1.f) apply_all([&](float y) { return leaky<true>(y, slope); });
-    else apply_all([&](float y) { return leaky<false>(y, slope); });
+    if (slope <= 1.f)
+        fwd_fused_apply<DT, VEC, T, R, STRIP, true>(xz, g, c, tid2, keep, mean_hi, scale, bshift, slope);
+    else
+        fwd_fused_apply<DT, VEC, T, R, STRIP, false>(xz, g, c, tid2, keep, mean_hi, scale, bshift, slope);
 }
 
 // Backward of one channel per block (sums of dy and dy*xhat, dgamma, dbeta,
@@ -883,7 +928,18 @@ __device__ __forceinline__ void bwd_fused_channel(const void* __restrict__ z,
     };
 #pragma unroll
     for (int k = 0; k < R; ++k) {
-        if (STRIP || tid + k * T < g.vchan) accumulate(kz[k], kg[k]);
+        if (STRIP || tid + k * T < g.vchan) {
+            float tz[VEC], tg[VEC];
+            unpack<DT, VEC>(kz[k], tz);
+            unpack<DT, VEC>(kg[k], tg);
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) {
+                float dy, xhat;
+                el(tz[e], tg[e], dy, xhat);
+                sdy += dy;
+                sdyx = fmaf(dy, xhat, sdyx);
+            }
+        }
         sched_fence();
     }
     acc_dy = sdy;
@@ -949,7 +1005,19 @@ __device__ __forceinline__ void bwd_fused_channel(const void* __restrict__ z,
             strip_next<T>(g, sq);
         } else {
             const uint32_t v = tid2 + k * T;
-            if (v < g.vchan) emit(kz[k], kg[k], access_index(g, cbase, v));
+            if (v < g.vchan) {
+                const uint64_t i1 = access_index(g, cbase, v);
+                float tz[VEC], tg[VEC];
+                unpack<DT, VEC>(kz[k], tz);
+                unpack<DT, VEC>(kg[k], tg);
+#pragma unroll
+                for (int e = 0; e < VEC; ++e) {
+                    float dy, xhat;
+                    el(tz[e], tg[e], dy, xhat);
+                    tg[e] = fmaf(ca, dy, fmaf(cb, xhat, cc));
+                }
+                store_vec<DT, VEC, kHintBwdApplyStore>(dzdx, i1, tg);
+            }
         }
         sched_fence();
     }
@@ -1198,7 +1266,8 @@ size_t fused_lds(int blocks_per_cu) {
     return kLdsPerCU / blocks_per_cu - 2048;  // leaves room for the kernels' own reduction buffers
 }
 
-// Candidate (T, R) in order of preference: the first whose threads hold the
+// Candidate (T, R) in order of preference (each one has a kernel built in
+// launch_fwd_fused / launch_bwd_fused): the first whose threads hold the
 // whole channel is used; larger channels take the last entry and re-read
 // the remainder.  The backward holds two tensors, so its largest blocks keep
 // half as many accesses per thread.
@@ -1240,11 +1309,8 @@ bool launch_fwd_fused(void* xz, const Geom& g, const FusedPlan& fp, const FwdPar
     const size_t lds = fused_lds(kFusedFwdBlocksPerCU);
     IABN_FUSED_CASE(fwd_fused_kernel, 256, 4, xz, g, prm)
     IABN_FUSED_CASE(fwd_fused_kernel, 512, 4, xz, g, prm)
-    IABN_FUSED_CASE(fwd_fused_kernel, 1024, 4, xz, g, prm)
     IABN_FUSED_CASE(fwd_fused_kernel, 256, 16, xz, g, prm)
-    IABN_FUSED_CASE(fwd_fused_kernel, 512, 8, xz, g, prm)
     IABN_FUSED_CASE(fwd_fused_kernel, 512, 16, xz, g, prm)
-    IABN_FUSED_CASE(fwd_fused_kernel, 1024, 8, xz, g, prm)
     IABN_FUSED_CASE(fwd_fused_kernel, 1024, 16, xz, g, prm)
     return false;
 }
@@ -1257,9 +1323,7 @@ bool launch_bwd_fused(const void* z, void* dzdx, const Geom& g, const FusedPlan&
     const size_t lds = fused_lds(kFusedBwdBlocksPerCU);
     IABN_FUSED_CASE(bwd_fused_kernel, 256, 4, z, dzdx, g, prm)
     IABN_FUSED_CASE(bwd_fused_kernel, 512, 4, z, dzdx, g, prm)
-    IABN_FUSED_CASE(bwd_fused_kernel, 1024, 4, z, dzdx, g, prm)
     IABN_FUSED_CASE(bwd_fused_kernel, 256, 16, z, dzdx, g, prm)
-    IABN_FUSED_CASE(bwd_fused_kernel, 512, 8, z, dzdx, g, prm)
     IABN_FUSED_CASE(bwd_fused_kernel, 512, 16, z, dzdx, g, prm)
     IABN_FUSED_CASE(bwd_fused_kernel, 1024, 8, z, dzdx, g, prm)
     return false;
