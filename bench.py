@@ -14,10 +14,16 @@ output stride 8; 33 BN layers in four shape groups, fp16 storage, fp32
 arithmetic), 1.14e9 elements per tensor.
 
 Output: one JSON line (see the keys below).  ``value`` is elements/s of the
-whole fwd+bwd step (elements = sum over layers of N*C*H*W).  ``roofline``
-covers the kernel with the largest share of the step, timed live with HIP
-events on the stream it runs on, in a separate pass that calls the two
-phases of each entry point with events between them.  ``cpu_baseline`` is the
+whole fwd+bwd step (elements = sum over layers of N*C*H*W).  ``kernels``
+gives each entry point's average launch duration, from HIP events recorded
+on the stream inside the timed steps (at each step's start, between its
+forward and backward passes, and at its end), with its algorithmic bytes
+(forward: read x, write z; backward: read z and dz, write dx).
+``roofline`` covers the one with the larger share of the step; its
+``traffic`` is the HBM bytes per launch that rocprofv3's FETCH_SIZE and
+WRITE_SIZE counters measured for the same kernels (scaled by a copy of
+known size), read from the committed profile summary and reported only
+while the kernel sources are unchanged since.  ``cpu_baseline`` is the
 double-precision oracle on the host's cores over whole layers of the same
 workload, bounded in time.
 """
@@ -55,11 +61,75 @@ def parse():
     ap.add_argument("--config", type=int, default=5, help="workload index (1-5)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="time budget of the oracle baseline (0 disables it)")
-    ap.add_argument("--no-kernel-pass", action="store_true",
-                    help="skip the per-kernel event pass (no roofline object)")
     ap.add_argument("--phase-kernels", action="store_true",
-                    help="also time the phase entry points (the streaming kernels)")
+                    help="also time the phase entry points (the streaming kernels), one by one")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="only copy MIB MiB device to device three times and exit (a kernel of "
+                         "known traffic, to scale hardware byte counters)")
     return ap.parse_args()
+
+
+def kernel_source_digest() -> str:
+    """sha256 of the sources libiabn.so is built from."""
+    import hashlib
+    h = hashlib.sha256()
+    for rel in ("paper_1712_02616_amd/csrc/iabn.hip", "paper_1712_02616_amd/csrc/divmagic.h",
+                "include/iabn.h"):
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "backbone_r101_os8_n8_f16_hbm_traffic.md")
+
+
+def measured_traffic(entry_point, config):
+    """HBM bytes per launch of an entry point's kernel, from the committed
+    rocprofv3 counter summary (FETCH_SIZE + WRITE_SIZE, scaled by a plain copy
+    of known size), or None when that summary does not cover this workload or
+    was taken from other kernel sources."""
+    if config != 5 or not os.path.exists(TRAFFIC_SUMMARY):
+        return None
+    fields = {}
+    for line in open(TRAFFIC_SUMMARY):
+        if line.startswith("- ") and ": " in line:
+            key, val = line[2:].split(": ", 1)
+            fields[key.strip()] = val.strip().strip("`")
+    if fields.get("source_sha256") != kernel_source_digest():
+        return None
+    val = fields.get("traffic_bytes_per_launch." + entry_point)
+    return int(val) if val else None
+
+
+def time_phases(lib, layers, refresh, check, stream, steps, b):
+    """The phase entry points (the streaming kernels) one by one, with events."""
+    import torch
+    tot_ms, tot_bytes, launches = {}, {}, {}
+    refresh()
+    torch.cuda.synchronize()
+    calls = ([x for L in layers for x in (("iabn_forward_stats", lib.iabn_forward_stats, L.stats, 1, L.E),
+                                          ("iabn_forward_apply", lib.iabn_forward_apply, L.fwd, 2, L.E))] +
+             [x for L in reversed(layers) for x in (("iabn_backward_reduce", lib.iabn_backward_reduce, L.reduce, 2, L.E),
+                                                    ("iabn_backward_apply", lib.iabn_backward_apply, L.bwd, 3, L.E))])
+    for _ in range(steps):
+        evs = []
+        for name, fn, cargs, bpe, E in calls:
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            check(fn(*cargs), name)
+            e1.record(stream)
+            evs.append((name, e0, e1, bpe * E * b))
+        torch.cuda.synchronize()
+        for name, e0, e1, nbytes in evs:
+            tot_ms[name] = tot_ms.get(name, 0.0) + e0.elapsed_time(e1)
+            tot_bytes[name] = tot_bytes.get(name, 0) + nbytes
+            launches[name] = launches.get(name, 0) + 1
+    return {name: {"avg_us": round(tot_ms[name] / launches[name] * 1e3, 3),
+                   "launches": launches[name],
+                   "alg_bytes_per_launch": tot_bytes[name] // launches[name],
+                   "achieved_gbps": round(tot_bytes[name] / (tot_ms[name] * 1e-3) / 1e9, 1)}
+            for name in tot_ms}
 
 
 class Layer:
@@ -75,6 +145,17 @@ def main():
     if os.environ.get("WORLD_SIZE", "1") != "1":
         print("bench.py runs as a single process on one GPU", file=sys.stderr)
         sys.exit(2)
+
+    if args.copy_calibration:
+        import torch
+        n = args.copy_calibration << 20
+        src = torch.empty(n, dtype=torch.uint8, device="cuda").fill_(1)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_calibration_bytes": n, "copies": 3}), flush=True)
+        return
 
     import paper_1712_02616_amd as iabn
 
@@ -162,23 +243,32 @@ def measure(lib, args):
             check(backward(*L.bwd), "iabn_backward")
 
     # ---------------------------------------------------------------- timed steps
+    # HIP events on the stream the kernels run on: at the start of each step,
+    # between its forward pass and its backward pass, and at the end.  Each
+    # pass is back-to-back launches of one entry point, so pass time / layers
+    # is that entry point's average launch duration over the timed region.
     refresh()
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
     refresh()
     torch.cuda.synchronize()
-    ev0 = torch.cuda.Event(enable_timing=True)
-    ev1 = torch.cuda.Event(enable_timing=True)
+    marks = [torch.cuda.Event(enable_timing=True) for _ in range(2 * args.steps + 1)]
     t0 = time.perf_counter()
-    ev0.record(stream)
-    for _ in range(args.steps):
-        step()
-    ev1.record(stream)
+    for i in range(args.steps):
+        marks[2 * i].record(stream)
+        for L in layers:
+            check(fwd_train(*L.fwd), "iabn_forward_train")
+        marks[2 * i + 1].record(stream)
+        for L in reversed(layers):
+            check(backward(*L.bwd), "iabn_backward")
+    marks[-1].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ms_per_step = wall * 1e3 / args.steps
-    ev_ms_per_step = ev0.elapsed_time(ev1) / args.steps
+    fwd_ms = sum(marks[2 * i].elapsed_time(marks[2 * i + 1]) for i in range(args.steps))
+    bwd_ms = sum(marks[2 * i + 1].elapsed_time(marks[2 * i + 2]) for i in range(args.steps))
+    ev_ms_per_step = (fwd_ms + bwd_ms) / args.steps
     value = E_total / (ms_per_step * 1e-3)
     sched_bytes = 8 * E_total * b
     floor_bytes = 5 * E_total * b
@@ -187,63 +277,26 @@ def measure(lib, args):
     log("timed %d steps: %.3f ms/step (events %.3f), %.3g elements/s, finite=%s"
         % (args.steps, ms_per_step, ev_ms_per_step, value, finite))
 
-    # ---------------------------------------------------------------- per-kernel pass
-    # The step's two entry points timed one by one with HIP events on the
-    # stream they run on.  On this workload each entry point is a single
-    # kernel (the channel-resident forward / backward); its algorithmic bytes
-    # are what the operation must move at least once: forward reads x and
-    # writes z (2 E b), backward reads z and dz and writes dx (3 E b).
-    roofline = None
-    kernels = None
+    launches = args.steps * len(layers)
+    kernels = {}
+    for name, tot_ms, bpe in (("iabn_forward_train", fwd_ms, 2), ("iabn_backward", bwd_ms, 3)):
+        nbytes = bpe * E_total * b * args.steps
+        kernels[name] = {"avg_us": round(tot_ms / launches * 1e3, 3), "launches": launches,
+                         "alg_bytes_per_launch": bpe * E_total * b // len(layers),
+                         "achieved_gbps": round(nbytes / (tot_ms * 1e-3) / 1e9, 1),
+                         "share_of_step": round(tot_ms / (fwd_ms + bwd_ms), 4)}
+    dom = max(kernels, key=lambda n: kernels[n]["share_of_step"])
+    k = kernels[dom]
+    roofline = {"bound": "hbm", "kernel": dom, "achieved": k["achieved_gbps"],
+                "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                "frac": round(k["achieved_gbps"] / HBM_PEAK_GBPS, 4),
+                "traffic": measured_traffic(dom, args.config)}
+    log("entry points: " + json.dumps(kernels))
+
+    # ---------------------------------------------------------------- phase kernels
     phase_kernels = None
-
-    def timed_pass(calls):
-        """calls: list of (name, fn, args, bytes_per_elem) per layer in step order."""
-        tot_ms, tot_bytes, launches = {}, {}, {}
-        refresh()
-        torch.cuda.synchronize()
-        for _ in range(args.steps):
-            evs = []
-            for name, fn, cargs, bpe, E in calls:
-                e0 = torch.cuda.Event(enable_timing=True)
-                e1 = torch.cuda.Event(enable_timing=True)
-                e0.record(stream)
-                check(fn(*cargs), name)
-                e1.record(stream)
-                evs.append((name, e0, e1, bpe * E * b))
-            torch.cuda.synchronize()
-            for name, e0, e1, nbytes in evs:
-                tot_ms[name] = tot_ms.get(name, 0.0) + e0.elapsed_time(e1)
-                tot_bytes[name] = tot_bytes.get(name, 0) + nbytes
-                launches[name] = launches.get(name, 0) + 1
-        out = {}
-        for name in tot_ms:
-            out[name] = {"avg_us": round(tot_ms[name] / launches[name] * 1e3, 3),
-                         "launches": launches[name],
-                         "alg_bytes_per_launch": tot_bytes[name] // launches[name],
-                         "achieved_gbps": round(tot_bytes[name] / (tot_ms[name] * 1e-3) / 1e9, 1),
-                         "share_of_pass": tot_ms[name]}
-        total = sum(tot_ms.values())
-        for name in out:
-            out[name]["share_of_pass"] = round(out[name]["share_of_pass"] / total, 4)
-        return out
-
-    if not args.no_kernel_pass:
-        entry = ([("iabn_forward_train", fwd_train, L.fwd, 2, L.E) for L in layers] +
-                 [("iabn_backward", backward, L.bwd, 3, L.E) for L in reversed(layers)])
-        kernels = timed_pass(entry)
-        dom = max(kernels, key=lambda n: kernels[n]["share_of_pass"])
-        k = kernels[dom]
-        roofline = {"bound": "hbm", "kernel": dom, "achieved": k["achieved_gbps"],
-                    "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                    "frac": round(k["achieved_gbps"] / HBM_PEAK_GBPS, 4), "traffic": None}
-        log("entry points: " + json.dumps(kernels))
     if args.phase_kernels:
-        phases = ([x for L in layers for x in (("iabn_forward_stats", lib.iabn_forward_stats, L.stats, 1, L.E),
-                                                ("iabn_forward_apply", lib.iabn_forward_apply, L.fwd, 2, L.E))] +
-                  [x for L in reversed(layers) for x in (("iabn_backward_reduce", lib.iabn_backward_reduce, L.reduce, 2, L.E),
-                                                          ("iabn_backward_apply", lib.iabn_backward_apply, L.bwd, 3, L.E))])
-        phase_kernels = timed_pass(phases)
+        phase_kernels = time_phases(lib, layers, refresh, check, stream, args.steps, b)
         log("phase entry points: " + json.dumps(phase_kernels))
 
     # ---------------------------------------------------------------- CPU baseline
