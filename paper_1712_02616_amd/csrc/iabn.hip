@@ -404,19 +404,55 @@ __global__ __launch_bounds__(kThreads) void fwd_apply_kernel(void* __restrict__ 
 
 // ---------------------------------------------------------------- backward
 
-// Per-element reconstruction from the stored output (Algorithm 2):
-//   dy = dz * f'(y) with f' = 1 where z >= 0, slope where z < 0
-//   y = f^-1(z) = z (z >= 0) or z / slope (z < 0)
-//   xhat = (y - beta) / gamma
-struct BwdElem {
-    float slope, inv_slope, beta, inv_gamma;
+// Per-element terms of Algorithm 2 from the stored output z, with the
+// per-channel constants folded in (exact in real arithmetic; formed in double
+// once per block):
+//   dy   = dz * f'(z)                   f' = 1 where z >= 0, slope where z < 0
+//   xhat = (f^-1(z) - beta) / gamma     = z * (z < 0 ? 1/(slope gamma) : 1/gamma) - beta/gamma
+// and, for the apply pass, with A = gamma/sqrt(var + eps), B = -A dgamma/m,
+// C = -A dbeta/m,
+//   dx   = A dy + B xhat + C
+//        = (z < 0 ? A slope : A) dz + (z < 0 ? B/(slope gamma) : B/gamma) z + (C - B beta/gamma).
+struct BwdReduceElem {
+    float slope, k_pos, k_neg, nb;
     __device__ __forceinline__ void operator()(float z, float dz, float& dy, float& xhat) const {
         const bool neg = z < 0.f;
-        const float y = neg ? z * inv_slope : z;
         dy = neg ? dz * slope : dz;
-        xhat = (y - beta) * inv_gamma;
+        xhat = fmaf(z, neg ? k_neg : k_pos, nb);
     }
 };
+
+__device__ __forceinline__ BwdReduceElem make_reduce_elem(float slope, float gamma, float beta) {
+    const double g = gamma, a = slope;
+    BwdReduceElem el;
+    el.slope = slope;
+    el.k_pos = static_cast<float>(1.0 / g);
+    el.k_neg = static_cast<float>(1.0 / (a * g));
+    el.nb = static_cast<float>(-static_cast<double>(beta) / g);
+    return el;
+}
+
+struct BwdApplyElem {
+    float a_pos, a_neg, b_pos, b_neg, c0;
+    __device__ __forceinline__ float operator()(float z, float dz) const {
+        const bool neg = z < 0.f;
+        return fmaf(neg ? a_neg : a_pos, dz, fmaf(neg ? b_neg : b_pos, z, c0));
+    }
+};
+
+__device__ __forceinline__ BwdApplyElem make_apply_elem(double A, double dgamma, double dbeta,
+                                                        double m, float slope, float gamma,
+                                                        float beta) {
+    const double B = -A * dgamma / m, C = -A * dbeta / m;
+    const double g = gamma, a = slope;
+    BwdApplyElem el;
+    el.a_pos = static_cast<float>(A);
+    el.a_neg = static_cast<float>(A * a);
+    el.b_pos = static_cast<float>(B / g);
+    el.b_neg = static_cast<float>(B / (a * g));
+    el.c0 = static_cast<float>(C - B * static_cast<double>(beta) / g);
+    return el;
+}
 
 // Sums of dy and dy*xhat of one wave's share of a (channel, slice): fp32 per
 // batch of U accesses, double across batches and lanes.
@@ -428,7 +464,7 @@ __global__ __launch_bounds__(kThreads) void bwd_reduce_kernel(const void* __rest
                                                               float slope,
                                                               Partial* __restrict__ part) {
     const Slice s = block_slice(g);
-    const BwdElem el = {slope, 1.0f / slope, beta[s.c], 1.0f / gamma[s.c]};
+    const BwdReduceElem el = make_reduce_elem(slope, gamma[s.c], beta[s.c]);
     const uint64_t cbase = static_cast<uint64_t>(s.c) * g.vrow;
     double acc_dy = 0.0, acc_dyx = 0.0;
     uint32_t v = s.lo + threadIdx.x;
@@ -516,23 +552,14 @@ __global__ __launch_bounds__(kThreads) void bwd_apply_kernel(const void* __restr
 
     double dbeta, dgamma;
     channel_sums(g, part, s.c, dbeta, dgamma);
-    const double m = g.m;
-    const double a = static_cast<double>(prm.gamma[s.c]) /
+    const double A = static_cast<double>(prm.gamma[s.c]) /
                      sqrt(static_cast<double>(prm.save_var[s.c]) + static_cast<double>(prm.eps));
-    const float ca = static_cast<float>(a);
-    const float cb = static_cast<float>(-a * dgamma / m);
-    const float cc = static_cast<float>(-a * dbeta / m);
+    const BwdApplyElem dx_of =
+        make_apply_elem(A, dgamma, dbeta, g.m, prm.slope, prm.gamma[s.c], prm.beta[s.c]);
     if (s.p == 0 && threadIdx.x == 0) {
         prm.dgamma[s.c] = static_cast<float>(dgamma);
         prm.dbeta[s.c] = static_cast<float>(dbeta);
     }
-    const BwdElem el = {prm.slope, 1.0f / prm.slope, prm.beta[s.c], 1.0f / prm.gamma[s.c]};
-
-    auto dx_of = [&](float zv, float gv) {
-        float dy, xhat;
-        el(zv, gv, dy, xhat);
-        return fmaf(ca, dy, fmaf(cb, xhat, cc));
-    };
 
     while (full) {
 #pragma unroll
@@ -893,7 +920,7 @@ __device__ __forceinline__ void bwd_fused_channel(const void* __restrict__ z,
     const uint32_t nstrips = STRIP ? g.vchan / T : 0;
     const raw16_t* const zv = static_cast<const raw16_t*>(z);
     const raw16_t* const gv = static_cast<const raw16_t*>(dzdx);
-    const BwdElem el = {prm.slope, 1.0f / prm.slope, prm.beta[c], 1.0f / prm.gamma[c]};
+    const BwdReduceElem el = make_reduce_elem(prm.slope, prm.gamma[c], prm.beta[c]);
 
     raw16_t kz[R], kg[R];
     StripPos sp = strip_begin(g, c);
@@ -975,12 +1002,9 @@ __device__ __forceinline__ void bwd_fused_channel(const void* __restrict__ z,
         opaque(kz[k]);
         opaque(kg[k]);
     }
-    const double m = g.m;
-    const double a = static_cast<double>(prm.gamma[c]) /
+    const double A = static_cast<double>(prm.gamma[c]) /
                      sqrt(static_cast<double>(prm.save_var[c]) + static_cast<double>(prm.eps));
-    const float ca = static_cast<float>(a);
-    const float cb = static_cast<float>(-a * dgamma / m);
-    const float cc = static_cast<float>(-a * dbeta / m);
+    const BwdApplyElem dx_of = make_apply_elem(A, dgamma, dbeta, g.m, prm.slope, prm.gamma[c], prm.beta[c]);
     if (tid == 0) {
         prm.dgamma[c] = static_cast<float>(dgamma);
         prm.dbeta[c] = static_cast<float>(dbeta);
@@ -990,11 +1014,7 @@ __device__ __forceinline__ void bwd_fused_channel(const void* __restrict__ z,
         unpack<DT, VEC>(rz, tz);
         unpack<DT, VEC>(rg, tg);
 #pragma unroll
-        for (int e = 0; e < VEC; ++e) {
-            float dy, xhat;
-            el(tz[e], tg[e], dy, xhat);
-            tg[e] = fmaf(ca, dy, fmaf(cb, xhat, cc));
-        }
+        for (int e = 0; e < VEC; ++e) tg[e] = dx_of(tz[e], tg[e]);
         store_vec<DT, VEC, kHintBwdApplyStore>(dzdx, idx, tg);
     };
     StripPos sq = strip_begin(g, c);
@@ -1011,11 +1031,7 @@ __device__ __forceinline__ void bwd_fused_channel(const void* __restrict__ z,
                 unpack<DT, VEC>(kz[k], tz);
                 unpack<DT, VEC>(kg[k], tg);
 #pragma unroll
-                for (int e = 0; e < VEC; ++e) {
-                    float dy, xhat;
-                    el(tz[e], tg[e], dy, xhat);
-                    tg[e] = fmaf(ca, dy, fmaf(cb, xhat, cc));
-                }
+                for (int e = 0; e < VEC; ++e) tg[e] = dx_of(tz[e], tg[e]);
                 store_vec<DT, VEC, kHintBwdApplyStore>(dzdx, i1, tg);
             }
         }
