@@ -821,6 +821,13 @@ __device__ __forceinline__ void fwd_fused_channel(void* __restrict__ xz, const G
     const uint32_t tid = threadIdx.x;
     const uint32_t nstrips = STRIP ? g.vchan / T : 0;
     raw16_t* const xv = static_cast<raw16_t*>(xz);
+    // Per-channel inputs before the data loads (see bwd_fused_channel).
+    const float gamma_c = prm.gamma[c], beta_c = prm.beta[c];
+    float rm_c = 0.f, rv_c = 0.f;
+    if (tid == 0) {
+        rm_c = prm.running_mean[c];
+        rv_c = prm.running_var[c];
+    }
 
     raw16_t keep[R];
     StripPos sp = strip_begin(g, c);
@@ -885,22 +892,21 @@ __device__ __forceinline__ void fwd_fused_channel(void* __restrict__ xz, const G
     opaque(tid2);
 #pragma unroll
     for (int k = 0; k < R; ++k) opaque(keep[k]);
-    const double scale_d = static_cast<double>(prm.gamma[c]) / sqrt(var + static_cast<double>(prm.eps));
+    const double scale_d = static_cast<double>(gamma_c) / sqrt(var + static_cast<double>(prm.eps));
     const float mean_hi = static_cast<float>(mean);
     const double mean_lo = mean - static_cast<double>(mean_hi);
     const float scale = static_cast<float>(scale_d);
     // (x - mu) * scale + beta with mu = mean_hi + mean_lo: the low part goes into the shift.
-    const float bshift = static_cast<float>(static_cast<double>(prm.beta[c]) - mean_lo * scale_d);
+    const float bshift = static_cast<float>(static_cast<double>(beta_c) - mean_lo * scale_d);
     const float slope = prm.slope;
     if (tid == 0) {
         const double mom = prm.momentum;
         const double m = g.m;
         prm.save_mean[c] = mean_hi;
         prm.save_var[c] = static_cast<float>(var);
-        prm.running_mean[c] = static_cast<float>(
-            (1.0 - mom) * static_cast<double>(prm.running_mean[c]) + mom * mean);
-        prm.running_var[c] = static_cast<float>(
-            (1.0 - mom) * static_cast<double>(prm.running_var[c]) + mom * var * (m / (m - 1.0)));
+        prm.running_mean[c] = static_cast<float>((1.0 - mom) * static_cast<double>(rm_c) + mom * mean);
+        prm.running_var[c] = static_cast<float>((1.0 - mom) * static_cast<double>(rv_c) +
+                                                mom * var * (m / (m - 1.0)));
     }
 
     if (slope <= 1.f)
@@ -920,7 +926,10 @@ __device__ __forceinline__ void bwd_fused_channel(const void* __restrict__ z,
     const uint32_t nstrips = STRIP ? g.vchan / T : 0;
     const raw16_t* const zv = static_cast<const raw16_t*>(z);
     const raw16_t* const gv = static_cast<const raw16_t*>(dzdx);
-    const BwdReduceElem el = make_reduce_elem(prm.slope, prm.gamma[c], prm.beta[c]);
+    // All per-channel inputs first: a load issued after the data loads would
+    // put another memory round trip after the reduction barrier.
+    const float gamma_c = prm.gamma[c], beta_c = prm.beta[c], var_c = prm.save_var[c];
+    const BwdReduceElem el = make_reduce_elem(prm.slope, gamma_c, beta_c);
 
     raw16_t kz[R], kg[R];
     StripPos sp = strip_begin(g, c);
@@ -939,6 +948,9 @@ __device__ __forceinline__ void bwd_fused_channel(const void* __restrict__ z,
             }
         }
     }
+    // fp32 within one access, fp64 across accesses (as the streaming reduce
+    // does per unrolled step): a channel's sums of dy cancel to near zero and
+    // an fp32 running sum over the whole register-resident part loses that.
     double acc_dy = 0.0, acc_dyx = 0.0;
     float sdy = 0.f, sdyx = 0.f;
     auto accumulate = [&](raw16_t rz, raw16_t rg) {
@@ -959,6 +971,8 @@ __device__ __forceinline__ void bwd_fused_channel(const void* __restrict__ z,
             float tz[VEC], tg[VEC];
             unpack<DT, VEC>(kz[k], tz);
             unpack<DT, VEC>(kg[k], tg);
+            sdy = 0.f;
+            sdyx = 0.f;
 #pragma unroll
             for (int e = 0; e < VEC; ++e) {
                 float dy, xhat;
@@ -966,11 +980,11 @@ __device__ __forceinline__ void bwd_fused_channel(const void* __restrict__ z,
                 sdy += dy;
                 sdyx = fmaf(dy, xhat, sdyx);
             }
+            acc_dy += sdy;
+            acc_dyx += sdyx;
         }
         sched_fence();
     }
-    acc_dy = sdy;
-    acc_dyx = sdyx;
     if constexpr (STRIP) {
 #pragma unroll 1
         for (uint32_t k = R; k < nstrips; ++k) {
@@ -1002,9 +1016,9 @@ __device__ __forceinline__ void bwd_fused_channel(const void* __restrict__ z,
         opaque(kz[k]);
         opaque(kg[k]);
     }
-    const double A = static_cast<double>(prm.gamma[c]) /
-                     sqrt(static_cast<double>(prm.save_var[c]) + static_cast<double>(prm.eps));
-    const BwdApplyElem dx_of = make_apply_elem(A, dgamma, dbeta, g.m, prm.slope, prm.gamma[c], prm.beta[c]);
+    const double A = static_cast<double>(gamma_c) /
+                     sqrt(static_cast<double>(var_c) + static_cast<double>(prm.eps));
+    const BwdApplyElem dx_of = make_apply_elem(A, dgamma, dbeta, g.m, prm.slope, gamma_c, beta_c);
     if (tid == 0) {
         prm.dgamma[c] = static_cast<float>(dgamma);
         prm.dbeta[c] = static_cast<float>(dbeta);
@@ -1053,10 +1067,12 @@ __device__ __forceinline__ void bwd_fused_channel(const void* __restrict__ z,
     }
 }
 
-// One block per channel: c = blockIdx.x.  (Looping a block over several
-// channels was measured slower: the loop made the compiler keep more values
-// live and halved occupancy, and overlapping one channel's stores with the
-// next one's loads gained nothing over the hardware's own block scheduling.)
+// One block per channel: c = blockIdx.x.  (Blocks that loop over several
+// channels were measured slower, both plainly and with the next channel
+// prefetched into a second register buffer: the second buffer limits a CU to
+// one block, and at that occupancy the per-channel reduce-barrier-apply chain
+// costs more than the overlap of one channel's stores with the next one's
+// loads gains.)
 template <int DT, int VEC, int T, int R, bool STRIP>
 __global__ __launch_bounds__(T) void fwd_fused_kernel(void* __restrict__ xz, Geom g,
                                                       FwdParams prm) {

@@ -84,6 +84,12 @@ EDGE_CASES = [
     Case("large_mean_f32", 8, 16, 1024, "f32", 25, x_shift=1000.0),
     Case("eps_large_bf16", 4, 16, 96, "bf16", 26, eps=0.5),
     Case("momentum_one_f32", 2, 4, 40, "f32", 27, momentum=1.0),
+    # Many channels at the strip-addressed fused shapes (a channel is exactly
+    # R strips of T accesses), including T = 256 with 16 strips.
+    Case("manych_c600_f16", 8, 600, 4096, "f16", 28, dz_std=0.1, gamma_sign=True),
+    Case("manych_c1300_bf16", 4, 1300, 8192, "bf16", 29, dz_std=0.1),
+    Case("manych_c520_f32", 4, 520, 4096, "f32", 30, dz_std=0.1),
+    Case("manych_t256_c512_f16", 16, 512, 2048, "f16", 31, dz_std=0.1),
 ]
 ALL_CASES = CONFIG_CASES + EDGE_CASES
 
