@@ -61,8 +61,14 @@ def _load():
         fn = getattr(lib, name)
         fn.argtypes = [P, P, I, I, I, P, P, P, D, D, P, P, P]
         fn.restype = None
-    lib.oracle_backward_standard.argtypes = [P, P, I, I, I, P, P, P, P, D, D, P, P, P]
+    lib.oracle_backward_standard.argtypes = [P, P, P, I, I, I, P, P, P, P, D, D, P, P, P]
     lib.oracle_backward_standard.restype = None
+    lib.oracle_normalize.argtypes = [P, I, I, I, P, P, D, P]
+    lib.oracle_normalize.restype = None
+    lib.oracle_scale_shift_act.argtypes = [P, I, I, I, P, P, D, P]
+    lib.oracle_scale_shift_act.restype = None
+    lib.oracle_backward_from_xhat.argtypes = [P, P, I, I, I, P, P, P, D, D, P, P, P]
+    lib.oracle_backward_from_xhat.restype = None
     lib.oracle_num_threads.argtypes = []
     lib.oracle_num_threads.restype = ctypes.c_int
     _lib = lib
@@ -155,17 +161,53 @@ def backward_ii(z, dz, gamma, beta, var, eps, slope):
     return _backward_from_z(_load().oracle_backward_ii, z, dz, gamma, beta, var, eps, slope)
 
 
-def backward_standard(x, dz, gamma, beta, mean, var, eps, slope):
-    """Standard BN + activation backward from the stored input x (Sec. 3.2)."""
+def backward_standard(x, dz, gamma, beta, mean, var, eps, slope, z=None):
+    """Standard BN + activation backward from the stored input x (Sec. 3.2).
+
+    With ``z`` (the block's stored output) the activation's derivative comes
+    from the sign of z; otherwise from the recomputed y.
+    """
     x, dz = _f64(x), _f64(dz)
     N, C, HW = _shape(x)
+    zp = None
+    if z is not None:
+        z = _f64(z)
+        if z.shape != x.shape:
+            raise ValueError("x and z shapes differ")
+        zp = _ptr(z)
     dx = np.empty_like(x)
     dg = np.empty(C)
     db = np.empty(C)
-    _load().oracle_backward_standard(_ptr(x), _ptr(dz), N, C, HW, _ptr(_f64(gamma)),
+    _load().oracle_backward_standard(_ptr(x), zp, _ptr(dz), N, C, HW, _ptr(_f64(gamma)),
                                      _ptr(_f64(beta)), _ptr(_f64(mean)), _ptr(_f64(var)),
                                      float(eps), float(slope), _ptr(dx), _ptr(dg), _ptr(db))
     return dict(dx=dx, dgamma=dg, dbeta=db)
+
+
+def normalize(x, mean, var, eps):
+    """xhat = (x - mu)/sqrt(sigma^2 + eps) of Eq. (1), for given statistics."""
+    x = _f64(x)
+    N, C, HW = _shape(x)
+    xh = np.empty_like(x)
+    _load().oracle_normalize(_ptr(x), N, C, HW, _ptr(_f64(mean)), _ptr(_f64(var)), float(eps),
+                             _ptr(xh))
+    return xh
+
+
+def scale_shift_act(xhat, gamma, beta, slope):
+    """z = f(gamma*xhat + beta): the checkpointing's recomputation (Sec. 3.2)."""
+    xhat = _f64(xhat)
+    N, C, HW = _shape(xhat)
+    z = np.empty_like(xhat)
+    _load().oracle_scale_shift_act(_ptr(xhat), N, C, HW, _ptr(_f64(gamma)), _ptr(_f64(beta)),
+                                   float(slope), _ptr(z))
+    return z
+
+
+def backward_from_xhat(xhat, dz, gamma, beta, var, eps, slope):
+    """Backward from the stored xhat (BN* of the proposed checkpointing, Sec. 3.2)."""
+    return _backward_from_z(_load().oracle_backward_from_xhat, xhat, dz, gamma, beta, var, eps,
+                            slope)
 
 
 def num_threads() -> int:

@@ -24,7 +24,14 @@
  *                                 forward, equality with three other
  *                                 formulations, closed-form invariants
  *   oracle_backward_ii            pinned: as above
- *   oracle_backward_standard      pinned: as above
+ *   oracle_backward_standard      pinned: as above; with z given, equal to the
+ *                                 backward from z and y-based form where signs agree
+ *   oracle_normalize              pinned: closed form, invariants (sum xhat = 0,
+ *                                 mean xhat^2 = sigma^2/(sigma^2 + eps))
+ *   oracle_scale_shift_act        pinned: equals the training forward's z on
+ *                                 the normalised input; dyadic exact case
+ *   oracle_backward_from_xhat     pinned: central finite differences, equality
+ *                                 with the backward from z and from x
  *   oracle_leaky_relu(_inv)       pinned: exact round trip for dyadic slopes
  */
 #include <math.h>
@@ -233,16 +240,18 @@ void oracle_backward_ii(const double *z, const double *dz, int64_t N, int64_t C,
 }
 
 /* Backward of the standard BN + activation block (Sec. 3.2, "Standard"), which
- * keeps the BN input x and the batch mean as well as the variance.  The
- * activation's derivative is taken on the recomputed y, and the BN gradient is
+ * keeps the BN input x and the batch mean as well as the variance.  That block
+ * also keeps the activation's output z for the activation's backward: when z
+ * is given, the derivative of f is taken from it (as in the backward from z,
+ * 1 where z >= 0); with z == NULL it is taken on the recomputed y.  The BN gradient is
  * assembled with the chain rule of the original BatchNorm paper as laid out in
  * the Appendix: dL/dxhat_j = dL/dy_j * gamma,
  *   dL/dsigma^2 = sum_j dL/dxhat_j * (x_j - mu) * (-1/2) (sigma^2 + eps)^(-3/2),
  *   dL/dmu      = -sum_j dL/dxhat_j / sqrt(sigma^2 + eps)
  *                 + dL/dsigma^2 * sum_j (-2 (x_j - mu)) / m,
  *   dL/dx_i = dL/dxhat_i / sqrt(sigma^2 + eps) + dL/dsigma^2 * 2 (x_i - mu) / m + dL/dmu / m. */
-void oracle_backward_standard(const double *x, const double *dz, int64_t N, int64_t C,
-                              int64_t HW, const double *gamma, const double *beta,
+void oracle_backward_standard(const double *x, const double *z, const double *dz, int64_t N,
+                              int64_t C, int64_t HW, const double *gamma, const double *beta,
                               const double *mean, const double *var, double eps,
                               double slope, double *dx, double *dgamma, double *dbeta) {
     const double m = (double)(N * HW);
@@ -258,7 +267,8 @@ void oracle_backward_standard(const double *x, const double *dz, int64_t N, int6
                 const double xc = x[k] - mean[c];
                 const double xhat = xc / denom;
                 const double y = gamma[c] * xhat + beta[c];
-                const double dy = dz[k] * ((y >= 0.0) ? 1.0 : slope);
+                const double dy = dz[k] * (z ? leaky_relu_slope_from_z(z[k], slope)
+                                             : ((y >= 0.0) ? 1.0 : slope));
                 const double dxhat = dy * gamma[c];
                 csum_add(&sdy, dy);
                 csum_add(&sdyx, dy * xhat);
@@ -273,11 +283,79 @@ void oracle_backward_standard(const double *x, const double *dz, int64_t N, int6
                 const size_t k = IDX(n, c, i);
                 const double xc = x[k] - mean[c];
                 const double y = gamma[c] * xc / denom + beta[c];
-                const double dy = dz[k] * ((y >= 0.0) ? 1.0 : slope);
+                const double dy = dz[k] * (z ? leaky_relu_slope_from_z(z[k], slope)
+                                             : ((y >= 0.0) ? 1.0 : slope));
                 const double dxhat = dy * gamma[c];
                 dx[k] = dxhat / denom + dvar * 2.0 * xc / m + dmu / m;
             }
         dgamma[c] = csum_value(&sdyx);
         dbeta[c] = csum_value(&sdy);
+    }
+}
+
+/* The normalised input of Eq. (1), xhat = (x - mu)/sqrt(sigma^2 + eps), for
+ * given per-channel mu and sigma^2: what the proposed checkpointing keeps for
+ * the backward (Sec. 3.2, "Checkpointing (proposed version)"). */
+void oracle_normalize(const double *x, int64_t N, int64_t C, int64_t HW, const double *mean,
+                      const double *var, double eps, double *xhat) {
+    int64_t c;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (c = 0; c < C; ++c) {
+        const double denom = sqrt(var[c] + eps);
+        for (int64_t n = 0; n < N; ++n)
+            for (int64_t i = 0; i < HW; ++i) {
+                const size_t k = IDX(n, c, i);
+                xhat[k] = (x[k] - mean[c]) / denom;
+            }
+    }
+}
+
+/* z = f(pi(xhat)) = f(gamma*xhat + beta): the recomputation of z from the
+ * stored xhat in the backward of the proposed checkpointing (Sec. 3.2). */
+void oracle_scale_shift_act(const double *xhat, int64_t N, int64_t C, int64_t HW,
+                            const double *gamma, const double *beta, double slope, double *z) {
+    int64_t c;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (c = 0; c < C; ++c)
+        for (int64_t n = 0; n < N; ++n)
+            for (int64_t i = 0; i < HW; ++i) {
+                const size_t k = IDX(n, c, i);
+                z[k] = oracle_leaky_relu(gamma[c] * xhat[k] + beta[c], slope);
+            }
+}
+
+/* Backward of the proposed checkpointing from the stored xhat (BN* of
+ * Sec. 3.2, with the BN backward of Sec. 3.3): y = gamma*xhat + beta,
+ * dy = dz * f'(y) (1 for y >= 0, slope otherwise),
+ *   dbeta = sum dy,  dgamma = sum dy*xhat,
+ *   dx = (dy - dgamma*xhat/m - dbeta/m) * gamma/sqrt(sigma^2 + eps). */
+void oracle_backward_from_xhat(const double *xhat, const double *dz, int64_t N, int64_t C,
+                               int64_t HW, const double *gamma, const double *beta,
+                               const double *var, double eps, double slope, double *dx,
+                               double *dgamma, double *dbeta) {
+    const double m = (double)(N * HW);
+    int64_t c;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (c = 0; c < C; ++c) {
+        csum_t sdy = {0.0, 0.0}, sdyx = {0.0, 0.0};
+        for (int64_t n = 0; n < N; ++n)
+            for (int64_t i = 0; i < HW; ++i) {
+                const size_t k = IDX(n, c, i);
+                const double y = gamma[c] * xhat[k] + beta[c];
+                const double dy = dz[k] * ((y >= 0.0) ? 1.0 : slope);
+                csum_add(&sdy, dy);
+                csum_add(&sdyx, dy * xhat[k]);
+            }
+        const double db = csum_value(&sdy), dg = csum_value(&sdyx);
+        const double scale = gamma[c] / sqrt(var[c] + eps);
+        for (int64_t n = 0; n < N; ++n)
+            for (int64_t i = 0; i < HW; ++i) {
+                const size_t k = IDX(n, c, i);
+                const double y = gamma[c] * xhat[k] + beta[c];
+                const double dy = dz[k] * ((y >= 0.0) ? 1.0 : slope);
+                dx[k] = (dy - dg * xhat[k] / m - db / m) * scale;
+            }
+        dgamma[c] = dg;
+        dbeta[c] = db;
     }
 }

@@ -340,3 +340,115 @@ def test_backward_tie_at_zero_takes_identity_branch():
     assert bw["dbeta"][0] == 1.0 + 2.0 + 4.0 + 0.25 * 8.0
     bw2 = oracle.backward_ii(z, dz, [1.0], [0.0], [1.0], EPS, 0.25)
     assert bw2["dbeta"][0] == bw["dbeta"][0]
+
+
+# ---------------------------------------------------------------- comparison blocks (Sec. 3.2)
+
+
+def test_normalize_closed_form():
+    """A channel of m values k +- d (half each) has mu = k and sigma^2 = d^2, so
+    xhat = +-d/sqrt(d^2 + eps) exactly (Eq. 1)."""
+    d, k, eps = 0.75, 3.0, 0.25
+    x = np.array([k + d, k - d] * 4, dtype=np.float64).reshape(2, 1, 4)
+    xh = oracle.normalize(x, [k], [d * d], eps)
+    expect = np.where(x > k, 1.0, -1.0) * d / np.sqrt(d * d + eps)
+    np.testing.assert_array_equal(xh, expect)
+
+
+def test_normalize_invariants():
+    """With the batch statistics, per channel sum xhat = 0 and
+    (1/m) sum xhat^2 = sigma^2/(sigma^2 + eps)."""
+    x, _, _, _ = _random_layer(3, 7, 33, seed=51)
+    eps = 0.1
+    mean, var = oracle.batch_stats(x)
+    xh = oracle.normalize(x, mean, var, eps)
+    m = 3 * 33
+    np.testing.assert_allclose(xh.sum(axis=(0, 2)), 0.0, atol=1e-12)
+    np.testing.assert_allclose((xh ** 2).sum(axis=(0, 2)) / m, var / (var + eps), rtol=1e-12)
+
+
+def test_scale_shift_act_equals_forward_z():
+    """f(gamma*xhat + beta) on xhat of the batch statistics is the training
+    forward's z (Algorithm 1); with dyadic gamma, beta, slope it is exact."""
+    x, _, g, b = _random_layer(2, 5, 24, seed=52, gamma_sign=True)
+    C = 5
+    fw = oracle.forward_train(x, g, b, np.zeros(C), np.ones(C), EPS, 0.1, SLOPE)
+    xh = oracle.normalize(x, fw["mean"], fw["var"], EPS)
+    z = oracle.scale_shift_act(xh, g, b, SLOPE)
+    assert _rel(z, fw["z"]) < 1e-14
+    xh2 = np.array([-2.0, -0.5, 0.0, 0.25, 3.0]).reshape(1, 1, 5)
+    z2 = oracle.scale_shift_act(xh2, [2.0], [-0.5], 0.25)
+    np.testing.assert_array_equal(z2.ravel(), [-1.125, -0.375, -0.125, 0.0, 5.5])
+
+
+def test_backward_from_xhat_finite_differences():
+    """The checkpointing backward from the stored xhat is dL/dx (and dL/dgamma,
+    dL/dbeta) of L = sum(dz * z(x)) by central differences."""
+    x, dz, g, b = _fd_inputs(100)
+    C = x.shape[1]
+    fw = oracle.forward_train(x, g, b, np.zeros(C), np.ones(C), EPS, 0.1, SLOPE)
+    xh = oracle.normalize(x, fw["mean"], fw["var"], EPS)
+    bw = oracle.backward_from_xhat(xh, dz, g, b, fw["var"], EPS, SLOPE)
+    h = 1e-6
+    fd = np.zeros_like(x)
+    for idx in np.ndindex(x.shape):
+        xp = x.copy()
+        xp[idx] += h
+        xm = x.copy()
+        xm[idx] -= h
+        fd[idx] = (_loss(xp, dz, g, b, EPS, SLOPE) - _loss(xm, dz, g, b, EPS, SLOPE)) / (2 * h)
+    assert _rel(bw["dx"], fd) < 1e-6
+    fdg = np.zeros(C)
+    fdb = np.zeros(C)
+    for c in range(C):
+        e = np.zeros(C)
+        e[c] = h
+        fdg[c] = (_loss(x, dz, g + e, b, EPS, SLOPE) - _loss(x, dz, g - e, b, EPS, SLOPE)) / (2 * h)
+        fdb[c] = (_loss(x, dz, g, b + e, EPS, SLOPE) - _loss(x, dz, g, b - e, EPS, SLOPE)) / (2 * h)
+    assert _rel(bw["dgamma"], fdg) < 1e-6
+    assert _rel(bw["dbeta"], fdb) < 1e-6
+
+
+@pytest.mark.parametrize("shape,seed,gsign", [((2, 16, 64), 61, False), ((4, 9, 49), 62, True)])
+def test_comparison_backwards_agree(shape, seed, gsign):
+    """The standard backward with f' from the stored z, and the checkpointing
+    backward from xhat, are the InPlace-ABN gradient (Sec. 3.2: the blocks
+    differ in what they store, not in what they compute)."""
+    x, dz, g, b = _random_layer(*shape, seed=seed, gamma_sign=gsign)
+    C = shape[1]
+    fw = oracle.forward_train(x, g, b, np.zeros(C), np.ones(C), EPS, 0.1, SLOPE)
+    ref = oracle.backward_i(fw["z"], dz, g, b, fw["var"], EPS, SLOPE)
+    st = oracle.backward_standard(x, dz, g, b, fw["mean"], fw["var"], EPS, SLOPE, z=fw["z"])
+    xh = oracle.normalize(x, fw["mean"], fw["var"], EPS)
+    ck = oracle.backward_from_xhat(xh, dz, g, b, fw["var"], EPS, SLOPE)
+    for k in ("dx", "dgamma", "dbeta"):
+        assert _rel(st[k], ref[k]) < 1e-11, k
+        assert _rel(ck[k], ref[k]) < 1e-11, k
+
+
+def test_standard_backward_takes_the_sign_of_the_stored_z():
+    """Given z, the standard backward's activation derivative follows z (the
+    block stores z for exactly that), not the recomputed y: a z whose sign
+    disagrees with y changes dbeta by (1 - a) dz at that element."""
+    x = np.array([-1.0, 1.0, -3.0, 3.0]).reshape(1, 1, 4)
+    dz = np.array([1.0, 2.0, 4.0, 8.0]).reshape(1, 1, 4)
+    mean, var = oracle.batch_stats(x)
+    a = 0.25
+    z_true = np.array([-0.25, 1.0, -0.75, 3.0]).reshape(1, 1, 4)  # signs of y for gamma=1, beta=0
+    z_flip = z_true.copy()
+    z_flip[0, 0, 0] = 0.0
+    by_y = oracle.backward_standard(x, dz, [1.0], [0.0], mean, var, EPS, a)
+    by_z = oracle.backward_standard(x, dz, [1.0], [0.0], mean, var, EPS, a, z=z_true)
+    flip = oracle.backward_standard(x, dz, [1.0], [0.0], mean, var, EPS, a, z=z_flip)
+    assert by_z["dbeta"][0] == by_y["dbeta"][0] == a * 1.0 + 2.0 + a * 4.0 + 8.0
+    assert flip["dbeta"][0] == by_z["dbeta"][0] + (1.0 - a) * 1.0
+
+
+def test_backward_from_xhat_sign_is_exact():
+    """The checkpointing backward decides f' on y = gamma*xhat + beta; for
+    values where gamma*xhat + beta is exactly 0 it takes the identity branch,
+    and the sign of a tiny nonzero y is kept."""
+    xh = np.array([0.5, 0.5 + 2.0 ** -40, 0.5 - 2.0 ** -40]).reshape(1, 1, 3)
+    dz = np.array([1.0, 2.0, 4.0]).reshape(1, 1, 3)
+    bw = oracle.backward_from_xhat(xh, dz, [2.0], [-1.0], [1.0], EPS, 0.25)
+    assert bw["dbeta"][0] == 1.0 + 2.0 + 0.25 * 4.0
