@@ -8,7 +8,9 @@
  * its output z for the backward pass: the forward overwrites x with z
  * (Algorithm 1), and the backward recovers y = f^-1(z) and
  * xhat = (y - beta)/gamma from z, then forms the BN gradient (Algorithm 2,
- * InPlace-ABN I, with the BN backward of Sec. 3.3).
+ * InPlace-ABN I, with the BN backward of Sec. 3.3).  Also InPlace-ABN II,
+ * and the two blocks the paper compares against (the standard block and the
+ * proposed checkpointing, Sec. 3.2), on the same kernels.
  *
  * Conventions shared by every entry point
  * ---------------------------------------
@@ -166,6 +168,94 @@ int iabn_backward_apply(const void *z, void *dz_dx, int dtype, const float *gamm
                         const float *beta, const float *save_var, float *dgamma, float *dbeta,
                         float eps, float slope, int64_t N, int64_t C, int64_t HW,
                         void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * Backward with InPlace-ABN II (Sec. 3.2 "In-Place Activated Batch
+ * Normalization II" and the BN-dagger gradients of the Appendix): the same
+ * arguments, outputs and in-place rule as iabn_backward, but the gradients
+ * are written in terms of y = f^-1(z) instead of xhat, so the per-element
+ * inversion of the scale-and-shift disappears:
+ *   dbeta  = sum_i dy_i
+ *   dgamma = (sum_i dy_i * y_i - beta * dbeta) / gamma
+ *   dx_i   = (dy_i - dbeta/m - (y_i - beta) * dgamma/(gamma*m)) * gamma/sqrt(sigma^2 + eps).
+ * Equal to iabn_backward in exact arithmetic; the rounding differs (the
+ * conversion of sum dy*y cancels when |beta| >> |gamma * xhat|).
+ */
+int iabn_backward_ii(const void *z, void *dz_dx, int dtype, const float *gamma,
+                     const float *beta, const float *save_var, float *dgamma, float *dbeta,
+                     float eps, float slope, int64_t N, int64_t C, int64_t HW, void *workspace,
+                     size_t workspace_bytes, void *stream);
+
+/*
+ * The standard building block of Sec. 3.2 (Fig. 2(a)), the baseline the
+ * method is measured against: batch normalisation and leaky ReLU that keep
+ * both the input x and the output z for the backward.
+ *
+ * iabn_std_forward_train: as iabn_forward_train, but out of place.
+ *   x              [N,C,HW] input, read only (kept for the backward).
+ *   z              [N,C,HW] out: z, the same values iabn_forward_train writes.
+ *   x and z must not overlap.  Other arguments as in iabn_forward_train.
+ *
+ * iabn_std_backward: the BN backward from x (Sec. 3.3, xhat = (x - mu)/sqrt(sigma^2 + eps))
+ * and the activation's backward from z (dy = dz * f'(y), f' from the sign of
+ * z as in iabn_backward).
+ *   x, z           [N,C,HW] the forward's input and output (read only).
+ *   dz_dx          in: dL/dz; out: dL/dx (in place).
+ *   save_mean, save_var
+ *                  [C] the batch mean and biased variance the forward saved.
+ *   dgamma, dbeta  [C] out, overwritten: dbeta = sum dy, dgamma = sum dy*xhat;
+ *   dx as in iabn_backward.  x, z and dz_dx must not overlap.
+ */
+int iabn_std_forward_train(const void *x, void *z, int dtype, const float *gamma,
+                           const float *beta, float *running_mean, float *running_var,
+                           float *save_mean, float *save_var, float eps, float momentum,
+                           float slope, int64_t N, int64_t C, int64_t HW, void *workspace,
+                           size_t workspace_bytes, void *stream);
+
+int iabn_std_backward(const void *x, const void *z, void *dz_dx, int dtype, const float *gamma,
+                      const float *beta, const float *save_mean, const float *save_var,
+                      float *dgamma, float *dbeta, float eps, float slope, int64_t N, int64_t C,
+                      int64_t HW, void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * The proposed checkpointing of Sec. 3.2 (Fig. 2(c)): the forward keeps only
+ * the normalised xhat; the backward recomputes z = f(gamma*xhat + beta) for
+ * the layers that need it and runs the BN backward from the stored xhat
+ * (BN*, which skips the normalisation step).
+ *
+ * iabn_ckpt_forward_train: statistics and running estimates as
+ * iabn_forward_train.
+ *   x_xhat         in: x; out: xhat = (x - mu)/sqrt(sigma^2 + eps), rounded to the
+ *                  storage type.
+ *   z              [N,C,HW] out: z = f(gamma*xhat + beta), formed from xhat as
+ *                  stored (so iabn_ckpt_recompute reproduces it bit for bit).
+ *   x_xhat and z must not overlap.
+ *
+ * iabn_ckpt_recompute: z = f(gamma*xhat + beta) from the stored xhat, out of
+ * place (xhat and z must not overlap).  No workspace, no statistics; slope > 0.
+ *
+ * iabn_ckpt_backward: the BN backward from the stored xhat; f' is taken from
+ * the sign of y = gamma*xhat + beta (one fused multiply-add, so the sign is
+ * that of the exact value; 0 takes the identity side).
+ *   xhat           [N,C,HW] read only.
+ *   dz_dx          in: dL/dz; out: dL/dx (in place).
+ *   save_var, dgamma, dbeta, eps, slope as in iabn_backward; dbeta = sum dy,
+ *   dgamma = sum dy*xhat, dx as in iabn_backward.
+ */
+int iabn_ckpt_forward_train(void *x_xhat, void *z, int dtype, const float *gamma,
+                            const float *beta, float *running_mean, float *running_var,
+                            float *save_mean, float *save_var, float eps, float momentum,
+                            float slope, int64_t N, int64_t C, int64_t HW, void *workspace,
+                            size_t workspace_bytes, void *stream);
+
+int iabn_ckpt_recompute(const void *xhat, void *z, int dtype, const float *gamma,
+                        const float *beta, float slope, int64_t N, int64_t C, int64_t HW,
+                        void *stream);
+
+int iabn_ckpt_backward(const void *xhat, void *dz_dx, int dtype, const float *gamma,
+                       const float *beta, const float *save_var, float *dgamma, float *dbeta,
+                       float eps, float slope, int64_t N, int64_t C, int64_t HW,
+                       void *workspace, size_t workspace_bytes, void *stream);
 
 #ifdef __cplusplus
 }

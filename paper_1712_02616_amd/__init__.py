@@ -27,7 +27,8 @@ __all__ = [
     "IabnError", "load", "library_path", "iabn_version", "iabn_status_string",
     "iabn_workspace_size", "iabn_forward_train", "iabn_forward_eval", "iabn_backward",
     "iabn_forward_stats", "iabn_forward_apply", "iabn_backward_reduce", "iabn_backward_apply",
-    "DTYPE_CODES",
+    "iabn_backward_ii", "iabn_std_forward_train", "iabn_std_backward", "iabn_ckpt_forward_train",
+    "iabn_ckpt_recompute", "iabn_ckpt_backward", "DTYPE_CODES",
 ]
 
 DTYPE_CODES = {torch.float32: 0, torch.float16: 1, torch.bfloat16: 2}
@@ -73,6 +74,12 @@ def declare(lib):
         "iabn_forward_apply": ([vp, i32, vp, vp, vp, vp, vp, vp, f32, f32, f32, i64, i64, i64, vp, sz, vp], i32),
         "iabn_backward_reduce": ([vp, vp, i32, vp, vp, f32, i64, i64, i64, vp, sz, vp], i32),
         "iabn_backward_apply": ([vp, vp, i32, vp, vp, vp, vp, vp, f32, f32, i64, i64, i64, vp, sz, vp], i32),
+        "iabn_backward_ii": ([vp, vp, i32, vp, vp, vp, vp, vp, f32, f32, i64, i64, i64, vp, sz, vp], i32),
+        "iabn_std_forward_train": ([vp, vp, i32, vp, vp, vp, vp, vp, vp, f32, f32, f32, i64, i64, i64, vp, sz, vp], i32),
+        "iabn_std_backward": ([vp, vp, vp, i32, vp, vp, vp, vp, vp, vp, f32, f32, i64, i64, i64, vp, sz, vp], i32),
+        "iabn_ckpt_forward_train": ([vp, vp, i32, vp, vp, vp, vp, vp, vp, f32, f32, f32, i64, i64, i64, vp, sz, vp], i32),
+        "iabn_ckpt_recompute": ([vp, vp, i32, vp, vp, f32, i64, i64, i64, vp], i32),
+        "iabn_ckpt_backward": ([vp, vp, i32, vp, vp, vp, vp, vp, f32, f32, i64, i64, i64, vp, sz, vp], i32),
     }
     for name, (args, res) in sig.items():
         fn = getattr(lib, name)
@@ -191,6 +198,106 @@ def iabn_backward(z, dz_dx, gamma, beta, save_var, dgamma, dbeta, eps=1e-5, slop
     rc = load().iabn_backward(_ptr(z), _ptr(dz_dx), code, *args, float(eps), float(slope), N, C, HW,
                               wp, wb, _stream(dev, stream))
     _check("iabn_backward", rc)
+    return dz_dx
+
+
+def _same(a, b, what_a, what_b):
+    shape = _nchw(a, what_a)
+    if _nchw(b, what_b) != shape or b.dtype != a.dtype or b.device != a.device:
+        raise ValueError("%s must match %s in shape, dtype and device" % (what_b, what_a))
+    return shape
+
+
+def iabn_backward_ii(z, dz_dx, gamma, beta, save_var, dgamma, dbeta, eps=1e-5, slope=0.01,
+                     workspace=None, stream=None):
+    """Backward with InPlace-ABN II (gradients in terms of y), in place over ``dz_dx``."""
+    N, C, HW = _same(z, dz_dx, "z", "dz_dx")
+    code = DTYPE_CODES[z.dtype]
+    dev = z.device
+    args = [_chan(t, C, dev, n) for t, n in ((gamma, "gamma"), (beta, "beta"),
+            (save_var, "save_var"), (dgamma, "dgamma"), (dbeta, "dbeta"))]
+    ws, wp, wb = _workspace(N, C, HW, code, dev, workspace)
+    rc = load().iabn_backward_ii(_ptr(z), _ptr(dz_dx), code, *args, float(eps), float(slope), N, C,
+                                 HW, wp, wb, _stream(dev, stream))
+    _check("iabn_backward_ii", rc)
+    return dz_dx
+
+
+def iabn_std_forward_train(x, z, gamma, beta, running_mean, running_var, save_mean, save_var,
+                           eps=1e-5, momentum=0.1, slope=0.01, workspace=None, stream=None):
+    """Standard block forward: ``x`` kept, ``z`` written; returns ``z``."""
+    N, C, HW = _same(x, z, "x", "z")
+    code = DTYPE_CODES[x.dtype]
+    dev = x.device
+    args = [_chan(t, C, dev, n) for t, n in ((gamma, "gamma"), (beta, "beta"),
+            (running_mean, "running_mean"), (running_var, "running_var"),
+            (save_mean, "save_mean"), (save_var, "save_var"))]
+    ws, wp, wb = _workspace(N, C, HW, code, dev, workspace)
+    rc = load().iabn_std_forward_train(_ptr(x), _ptr(z), code, *args, float(eps), float(momentum),
+                                       float(slope), N, C, HW, wp, wb, _stream(dev, stream))
+    _check("iabn_std_forward_train", rc)
+    return z
+
+
+def iabn_std_backward(x, z, dz_dx, gamma, beta, save_mean, save_var, dgamma, dbeta, eps=1e-5,
+                      slope=0.01, workspace=None, stream=None):
+    """Standard block backward from ``x`` (and the signs of ``z``), in place over ``dz_dx``."""
+    N, C, HW = _same(x, z, "x", "z")
+    _same(x, dz_dx, "x", "dz_dx")
+    code = DTYPE_CODES[x.dtype]
+    dev = x.device
+    args = [_chan(t, C, dev, n) for t, n in ((gamma, "gamma"), (beta, "beta"),
+            (save_mean, "save_mean"), (save_var, "save_var"), (dgamma, "dgamma"), (dbeta, "dbeta"))]
+    ws, wp, wb = _workspace(N, C, HW, code, dev, workspace)
+    rc = load().iabn_std_backward(_ptr(x), _ptr(z), _ptr(dz_dx), code, *args, float(eps),
+                                  float(slope), N, C, HW, wp, wb, _stream(dev, stream))
+    _check("iabn_std_backward", rc)
+    return dz_dx
+
+
+def iabn_ckpt_forward_train(x_xhat, z, gamma, beta, running_mean, running_var, save_mean,
+                            save_var, eps=1e-5, momentum=0.1, slope=0.01, workspace=None,
+                            stream=None):
+    """Checkpointing forward: xhat over ``x_xhat``, ``z`` written; returns ``z``."""
+    N, C, HW = _same(x_xhat, z, "x_xhat", "z")
+    code = DTYPE_CODES[x_xhat.dtype]
+    dev = x_xhat.device
+    args = [_chan(t, C, dev, n) for t, n in ((gamma, "gamma"), (beta, "beta"),
+            (running_mean, "running_mean"), (running_var, "running_var"),
+            (save_mean, "save_mean"), (save_var, "save_var"))]
+    ws, wp, wb = _workspace(N, C, HW, code, dev, workspace)
+    rc = load().iabn_ckpt_forward_train(_ptr(x_xhat), _ptr(z), code, *args, float(eps),
+                                        float(momentum), float(slope), N, C, HW, wp, wb,
+                                        _stream(dev, stream))
+    _check("iabn_ckpt_forward_train", rc)
+    return z
+
+
+def iabn_ckpt_recompute(xhat, z, gamma, beta, slope=0.01, stream=None):
+    """z = f(gamma*xhat + beta) from the stored xhat; returns ``z``."""
+    N, C, HW = _same(xhat, z, "xhat", "z")
+    code = DTYPE_CODES[xhat.dtype]
+    dev = xhat.device
+    g = _chan(gamma, C, dev, "gamma")
+    b = _chan(beta, C, dev, "beta")
+    rc = load().iabn_ckpt_recompute(_ptr(xhat), _ptr(z), code, g, b, float(slope), N, C, HW,
+                                    _stream(dev, stream))
+    _check("iabn_ckpt_recompute", rc)
+    return z
+
+
+def iabn_ckpt_backward(xhat, dz_dx, gamma, beta, save_var, dgamma, dbeta, eps=1e-5, slope=0.01,
+                       workspace=None, stream=None):
+    """Checkpointing backward from the stored xhat, in place over ``dz_dx``."""
+    N, C, HW = _same(xhat, dz_dx, "xhat", "dz_dx")
+    code = DTYPE_CODES[xhat.dtype]
+    dev = xhat.device
+    args = [_chan(t, C, dev, n) for t, n in ((gamma, "gamma"), (beta, "beta"),
+            (save_var, "save_var"), (dgamma, "dgamma"), (dbeta, "dbeta"))]
+    ws, wp, wb = _workspace(N, C, HW, code, dev, workspace)
+    rc = load().iabn_ckpt_backward(_ptr(xhat), _ptr(dz_dx), code, *args, float(eps), float(slope),
+                                   N, C, HW, wp, wb, _stream(dev, stream))
+    _check("iabn_ckpt_backward", rc)
     return dz_dx
 
 

@@ -316,15 +316,32 @@ struct FwdParams {
     float* running_var;
     float* save_mean;
     float* save_var;
+    void* out;  // z for kFwdOut and kFwdCkpt
     float eps, momentum, slope;
 };
 
-// z = f(gamma * (x - mu) / sqrt(var + eps) + beta), in place.  TRAIN: mu and
-// var are the batch statistics combined from the partials (slice 0 of each
-// channel also writes them out and updates the running estimates); otherwise
-// they are the running estimates.  mu is applied as a two-float sum
-// hi + lo, so x - mu keeps fp32 relative accuracy even when |mu| >> sigma.
-template <int DT, int VEC, int U, bool TRAIN>
+// Forward outputs.  kFwdInPlace: z over x (InPlace-ABN, Fig. 2(d)).
+// kFwdOut: z to a separate buffer, x kept (the standard block, Fig. 2(a)).
+// kFwdCkpt: xhat over x and z to a separate buffer (the proposed
+// checkpointing, Fig. 2(c)); z is formed from xhat as stored, so the
+// backward's recomputation of z from the stored xhat reproduces it exactly.
+constexpr int kFwdInPlace = 0;
+constexpr int kFwdOut = 1;
+constexpr int kFwdCkpt = 2;
+
+// A value rounded to the storage type and widened back.
+template <int DT>
+__device__ __forceinline__ float storage_round(float v) {
+    return static_cast<float>(static_cast<typename Elem<DT>::T>(v));
+}
+
+// z = f(gamma * (x - mu) / sqrt(var + eps) + beta).  TRAIN: mu and var are
+// the batch statistics combined from the partials (slice 0 of each channel
+// also writes them out and updates the running estimates); otherwise they
+// are the running estimates (inference, in place only).  mu is applied as a
+// two-float sum hi + lo, so x - mu keeps fp32 relative accuracy even when
+// |mu| >> sigma.
+template <int DT, int VEC, int U, bool TRAIN, int FM>
 __global__ __launch_bounds__(kThreads) void fwd_apply_kernel(void* __restrict__ xz, Geom g,
                                                              const Partial* __restrict__ part,
                                                              FwdParams prm) {
@@ -338,9 +355,9 @@ __global__ __launch_bounds__(kThreads) void fwd_apply_kernel(void* __restrict__ 
     bool full = v + (U - 1) * kThreads < s.hi;
     if (full) {
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
-            idx[u] = access_index(g, cbase, v + u * kThreads);
-            load_vec<DT, VEC, kHintFwdApplyLoad>(xz, idx[u], t[u]);
+        for (int q = 0; q < U; ++q) {
+            idx[q] = access_index(g, cbase, v + q * kThreads);
+            load_vec<DT, VEC, kHintFwdApplyLoad>(xz, idx[q], t[q]);
         }
     }
 
@@ -353,9 +370,12 @@ __global__ __launch_bounds__(kThreads) void fwd_apply_kernel(void* __restrict__ 
     }
     const float mean_hi = static_cast<float>(mean);
     const float mean_lo = static_cast<float>(mean - static_cast<double>(mean_hi));
-    const float scale = static_cast<float>(static_cast<double>(prm.gamma[s.c]) /
-                                           sqrt(var + static_cast<double>(prm.eps)));
-    const float shift = prm.beta[s.c];
+    const double invstd = 1.0 / sqrt(var + static_cast<double>(prm.eps));
+    const float gamma = prm.gamma[s.c], beta = prm.beta[s.c];
+    // kFwdCkpt normalises first (scale 1/sigma, shift beta applied after the
+    // rounding of xhat); the others fold gamma into the scale.
+    const float scale = static_cast<float>(FM == kFwdCkpt ? invstd : gamma * invstd);
+    const float shift = FM == kFwdCkpt ? 0.f : beta;
     const float slope = prm.slope;
     if constexpr (TRAIN) {
         if (s.p == 0 && threadIdx.x == 0) {
@@ -370,25 +390,35 @@ __global__ __launch_bounds__(kThreads) void fwd_apply_kernel(void* __restrict__ 
         }
     }
 
-    auto act = [&](float xv) {
-        const float y = fmaf((xv - mean_hi) - mean_lo, scale, shift);
-        return y >= 0.f ? y : slope * y;
+    auto act = [&](float y) { return y >= 0.f ? y : slope * y; };
+    // Writes the outputs of access i1 from its inputs r (overwritten).
+    auto emit = [&](float (&r)[VEC], uint64_t i1) {
+        if constexpr (FM == kFwdCkpt) {
+            float zv[VEC];
+#pragma unroll
+            for (int k = 0; k < VEC; ++k) {
+                r[k] = storage_round<DT>(fmaf((r[k] - mean_hi) - mean_lo, scale, shift));
+                zv[k] = act(fmaf(r[k], gamma, beta));
+            }
+            store_vec<DT, VEC, kHintFwdApplyStore>(xz, i1, r);
+            store_vec<DT, VEC, kHintFwdApplyStore>(prm.out, i1, zv);
+        } else {
+#pragma unroll
+            for (int k = 0; k < VEC; ++k) r[k] = act(fmaf((r[k] - mean_hi) - mean_lo, scale, shift));
+            store_vec<DT, VEC, kHintFwdApplyStore>(FM == kFwdOut ? prm.out : xz, i1, r);
+        }
     };
 
     while (full) {
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
-#pragma unroll
-            for (int k = 0; k < VEC; ++k) t[u][k] = act(t[u][k]);
-            store_vec<DT, VEC, kHintFwdApplyStore>(xz, idx[u], t[u]);
-        }
+        for (int q = 0; q < U; ++q) emit(t[q], idx[q]);
         v += U * kThreads;
         full = v + (U - 1) * kThreads < s.hi;
         if (full) {
 #pragma unroll
-            for (int u = 0; u < U; ++u) {
-                idx[u] = access_index(g, cbase, v + u * kThreads);
-                load_vec<DT, VEC, kHintFwdApplyLoad>(xz, idx[u], t[u]);
+            for (int q = 0; q < U; ++q) {
+                idx[q] = access_index(g, cbase, v + q * kThreads);
+                load_vec<DT, VEC, kHintFwdApplyLoad>(xz, idx[q], t[q]);
             }
         }
     }
@@ -396,141 +426,268 @@ __global__ __launch_bounds__(kThreads) void fwd_apply_kernel(void* __restrict__ 
         float r[VEC];
         const uint64_t i1 = access_index(g, cbase, v);
         load_vec<DT, VEC, kHintFwdApplyLoad>(xz, i1, r);
+        emit(r, i1);
+    }
+}
+
+// z = f(gamma * xhat + beta) from a stored xhat, out of place: the
+// recomputation step of the proposed checkpointing (Fig. 2(c)).
+template <int DT, int VEC>
+__global__ __launch_bounds__(kThreads) void recompute_kernel(const void* __restrict__ xhat,
+                                                             void* __restrict__ z, Geom g,
+                                                             const float* __restrict__ gamma,
+                                                             const float* __restrict__ beta,
+                                                             float slope) {
+    const Slice s = block_slice(g);
+    const uint64_t cbase = static_cast<uint64_t>(s.c) * g.vrow;
+    const float gm = gamma[s.c], bt = beta[s.c];
+    for (uint32_t v = s.lo + threadIdx.x; v < s.hi; v += kThreads) {
+        float r[VEC];
+        const uint64_t i1 = access_index(g, cbase, v);
+        load_vec<DT, VEC, kStream>(xhat, i1, r);
 #pragma unroll
-        for (int k = 0; k < VEC; ++k) r[k] = act(r[k]);
-        store_vec<DT, VEC, kHintFwdApplyStore>(xz, i1, r);
+        for (int k = 0; k < VEC; ++k) {
+            const float y = fmaf(r[k], gm, bt);
+            r[k] = y >= 0.f ? y : slope * y;
+        }
+        store_vec<DT, VEC, kStream>(z, i1, r);
     }
 }
 
 // ---------------------------------------------------------------- backward
 
-// Per-element terms of Algorithm 2 from the stored output z, with the
-// per-channel constants folded in (exact in real arithmetic; formed in double
-// once per block):
-//   dy   = dz * f'(z)                   f' = 1 where z >= 0, slope where z < 0
-//   xhat = (f^-1(z) - beta) / gamma     = z * (z < 0 ? 1/(slope gamma) : 1/gamma) - beta/gamma
-// and, for the apply pass, with A = gamma/sqrt(var + eps), B = -A dgamma/m,
-// C = -A dbeta/m,
-//   dx   = A dy + B xhat + C
-//        = (z < 0 ? A slope : A) dz + (z < 0 ? B/(slope gamma) : B/gamma) z + (C - B beta/gamma).
-struct BwdReduceElem {
-    float slope, k_pos, k_neg, nb;
-    __device__ __forceinline__ void operator()(float z, float dz, float& dy, float& xhat) const {
-        const bool neg = z < 0.f;
-        dy = neg ? dz * slope : dz;
-        xhat = fmaf(z, neg ? k_neg : k_pos, nb);
+// Backward formulations.  Each reads a stored tensor u (plus dz) and
+// recovers, per element, dy = dz * f'(y) and a weight w whose sum against dy
+// gives dgamma:
+//   kBwdFromZ     u = z (InPlace-ABN, Sec. 3.3, Algorithm 2).  f' from the
+//                 sign of z.  Formulation I: w = xhat = (f^-1(z) - beta)/gamma.
+//                 Formulation II (BN-dagger, the Appendix): w = y = f^-1(z),
+//                 dgamma = (sum dy*y - beta sum dy)/gamma per channel.
+//   kBwdFromXZ    u = x, plus the stored z for f' (the standard block of
+//                 Fig. 2(a), which keeps x and z): w = xhat = (x - mu)/sigma.
+//   kBwdFromXhat  u = xhat (the proposed checkpointing of Fig. 2(c)):
+//                 f' from the sign of y = gamma*xhat + beta, w = xhat.
+// With the per-channel constants folded in (exact in real arithmetic, formed
+// in double once per block) every formulation is
+//   w  = (u - off) * (neg ? k_neg : k_pos) + nb
+//   dx = A dy + B xhat + C        (A = gamma/sqrt(var + eps), B = -A dgamma/m, C = -A dbeta/m)
+//      = (neg ? a_neg : a_pos) dz + (neg ? b_neg : b_pos) (u - off) + c0
+// e.g. for formulation I: k_pos = 1/gamma, k_neg = 1/(slope gamma),
+// nb = -beta/gamma, b_pos = B/gamma, b_neg = B/(slope gamma),
+// c0 = C - B beta/gamma.
+constexpr int kBwdFromZ = 0;
+constexpr int kBwdFromXZ = 1;
+constexpr int kBwdFromXhat = 2;
+
+// The sign test of f'(y): y < 0.  kBwdFromZ and kBwdFromXZ test the stored z
+// (f preserves the sign and -0 stays on the identity side); kBwdFromXhat
+// forms y = fma(xhat, gamma, beta), whose single rounding keeps the sign of
+// the exact gamma*xhat + beta.
+template <int BM>
+struct BwdSign {
+    float gamma, beta;
+    __device__ __forceinline__ bool operator()(float u, float zv) const {
+        if constexpr (BM == kBwdFromZ) return u < 0.f;
+        else if constexpr (BM == kBwdFromXZ) return zv < 0.f;
+        else return fmaf(u, gamma, beta) < 0.f;
     }
 };
 
-__device__ __forceinline__ BwdReduceElem make_reduce_elem(float slope, float gamma, float beta) {
+template <int BM>
+struct BwdReduceElem {
+    BwdSign<BM> sign;
+    float slope, k_pos, k_neg, nb, off;
+    __device__ __forceinline__ void with_neg(bool neg, float u, float dz, float& dy,
+                                             float& w) const {
+        dy = neg ? dz * slope : dz;
+        if constexpr (BM == kBwdFromZ) w = fmaf(u, neg ? k_neg : k_pos, nb);
+        else if constexpr (BM == kBwdFromXZ) w = fmaf(u - off, k_pos, nb);
+        else w = u;
+    }
+    __device__ __forceinline__ void operator()(float u, float zv, float dz, float& dy,
+                                               float& w) const {
+        with_neg(sign(u, zv), u, dz, dy, w);
+    }
+};
+
+// Per-channel constants of the reduction.  ii selects formulation II
+// (w = y instead of xhat) for kBwdFromZ.
+template <int BM>
+__device__ __forceinline__ BwdReduceElem<BM> make_reduce_elem(float slope, float gamma, float beta,
+                                                              float mean, double invstd, bool ii) {
     const double g = gamma, a = slope;
-    BwdReduceElem el;
+    BwdReduceElem<BM> el;
+    el.sign.gamma = gamma;
+    el.sign.beta = beta;
     el.slope = slope;
-    el.k_pos = static_cast<float>(1.0 / g);
-    el.k_neg = static_cast<float>(1.0 / (a * g));
-    el.nb = static_cast<float>(-static_cast<double>(beta) / g);
+    el.k_pos = el.k_neg = 1.f;
+    el.nb = 0.f;
+    el.off = 0.f;
+    if constexpr (BM == kBwdFromZ) {
+        if (ii) {
+            el.k_neg = static_cast<float>(1.0 / a);
+        } else {
+            el.k_pos = static_cast<float>(1.0 / g);
+            el.k_neg = static_cast<float>(1.0 / (a * g));
+            el.nb = static_cast<float>(-static_cast<double>(beta) / g);
+        }
+    } else if constexpr (BM == kBwdFromXZ) {
+        el.off = mean;
+        el.k_pos = el.k_neg = static_cast<float>(invstd);
+    }
     return el;
 }
 
+template <int BM>
 struct BwdApplyElem {
-    float a_pos, a_neg, b_pos, b_neg, c0;
-    __device__ __forceinline__ float operator()(float z, float dz) const {
-        const bool neg = z < 0.f;
-        return fmaf(neg ? a_neg : a_pos, dz, fmaf(neg ? b_neg : b_pos, z, c0));
+    BwdSign<BM> sign;
+    float a_pos, a_neg, b_pos, b_neg, c0, off;
+    __device__ __forceinline__ float operator()(float u, float zv, float dz) const {
+        return with_neg(sign(u, zv), u, dz);
+    }
+    __device__ __forceinline__ float with_neg(bool neg, float u, float dz) const {
+        if constexpr (BM == kBwdFromZ)
+            return fmaf(neg ? a_neg : a_pos, dz, fmaf(neg ? b_neg : b_pos, u, c0));
+        else if constexpr (BM == kBwdFromXZ)
+            return fmaf(neg ? a_neg : a_pos, dz, fmaf(b_pos, u - off, c0));
+        else
+            return fmaf(neg ? a_neg : a_pos, dz, fmaf(b_pos, u, c0));
     }
 };
 
-__device__ __forceinline__ BwdApplyElem make_apply_elem(double A, double dgamma, double dbeta,
-                                                        double m, float slope, float gamma,
-                                                        float beta) {
+// dgamma from the two sums (formulation II converts sum dy*y), then the
+// apply constants.  sdyw is overwritten with dgamma.
+template <int BM>
+__device__ __forceinline__ BwdApplyElem<BM> make_apply_elem(double A, double& sdyw, double dbeta,
+                                                            double m, float slope, float gamma,
+                                                            float beta, float mean, double invstd,
+                                                            bool ii) {
+    const double g = gamma, a = slope, bt = beta;
+    if (BM == kBwdFromZ && ii) sdyw = (sdyw - bt * dbeta) / g;
+    const double dgamma = sdyw;
     const double B = -A * dgamma / m, C = -A * dbeta / m;
-    const double g = gamma, a = slope;
-    BwdApplyElem el;
+    BwdApplyElem<BM> el;
+    el.sign.gamma = gamma;
+    el.sign.beta = beta;
     el.a_pos = static_cast<float>(A);
     el.a_neg = static_cast<float>(A * a);
-    el.b_pos = static_cast<float>(B / g);
-    el.b_neg = static_cast<float>(B / (a * g));
-    el.c0 = static_cast<float>(C - B * static_cast<double>(beta) / g);
+    el.off = 0.f;
+    if constexpr (BM == kBwdFromZ) {
+        el.b_pos = static_cast<float>(B / g);
+        el.b_neg = static_cast<float>(B / (a * g));
+        el.c0 = static_cast<float>(C - B * bt / g);
+    } else if constexpr (BM == kBwdFromXZ) {
+        el.off = mean;
+        el.b_pos = el.b_neg = static_cast<float>(B * invstd);
+        el.c0 = static_cast<float>(C);
+    } else {
+        el.b_pos = el.b_neg = static_cast<float>(B);
+        el.c0 = static_cast<float>(C);
+    }
     return el;
 }
 
-// Sums of dy and dy*xhat of one wave's share of a (channel, slice): fp32 per
-// batch of U accesses, double across batches and lanes.
-template <int DT, int VEC, int U>
-__global__ __launch_bounds__(kThreads) void bwd_reduce_kernel(const void* __restrict__ z,
+struct BwdParams {
+    const float* gamma;
+    const float* beta;
+    const float* save_mean;  // kBwdFromXZ only
+    const float* save_var;
+    float* dgamma;
+    float* dbeta;
+    float eps, slope;
+    int ii;  // formulation II (kBwdFromZ only)
+};
+
+__device__ __forceinline__ double chan_invstd(const BwdParams& prm, uint32_t c) {
+    return 1.0 / sqrt(static_cast<double>(prm.save_var[c]) + static_cast<double>(prm.eps));
+}
+
+// Loads the z of access i1 for the sign test of kBwdFromXZ (nothing otherwise).
+template <int DT, int VEC, int HINT, int BM>
+__device__ __forceinline__ void load_sign(const void* __restrict__ zs, uint64_t i1,
+                                          float (&v)[VEC]) {
+    if constexpr (BM == kBwdFromXZ) {
+        load_vec<DT, VEC, HINT>(zs, i1, v);
+    } else {
+#pragma unroll
+        for (int k = 0; k < VEC; ++k) v[k] = 0.f;
+    }
+}
+
+// Sums of dy and dy*w of one wave's share of a (channel, slice): fp32 per
+// batch of U accesses, double across batches and lanes.  u is z, x or xhat
+// (see BwdSign); zs is the stored z for kBwdFromXZ.
+template <int DT, int VEC, int U, int BM>
+__global__ __launch_bounds__(kThreads) void bwd_reduce_kernel(const void* __restrict__ u,
+                                                              const void* __restrict__ zs,
                                                               const void* __restrict__ dz, Geom g,
-                                                              const float* __restrict__ gamma,
-                                                              const float* __restrict__ beta,
-                                                              float slope,
+                                                              BwdParams prm,
                                                               Partial* __restrict__ part) {
     const Slice s = block_slice(g);
-    const BwdReduceElem el = make_reduce_elem(slope, gamma[s.c], beta[s.c]);
+    const double invstd = BM == kBwdFromXZ ? chan_invstd(prm, s.c) : 1.0;
+    const BwdReduceElem<BM> el =
+        make_reduce_elem<BM>(prm.slope, prm.gamma[s.c], prm.beta[s.c],
+                             BM == kBwdFromXZ ? prm.save_mean[s.c] : 0.f, invstd, prm.ii != 0);
     const uint64_t cbase = static_cast<uint64_t>(s.c) * g.vrow;
-    double acc_dy = 0.0, acc_dyx = 0.0;
+    double acc_dy = 0.0, acc_dyw = 0.0;
     uint32_t v = s.lo + threadIdx.x;
     for (; v + (U - 1) * kThreads < s.hi; v += U * kThreads) {
-        float tz[U][VEC], tg[U][VEC];
+        float tu[U][VEC], tz[U][VEC], tg[U][VEC];
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const uint64_t i1 = access_index(g, cbase, v + u * kThreads);
-            load_vec<DT, VEC, kHintReduceLoad>(z, i1, tz[u]);
-            load_vec<DT, VEC, kHintReduceLoad>(dz, i1, tg[u]);
+        for (int q = 0; q < U; ++q) {
+            const uint64_t i1 = access_index(g, cbase, v + q * kThreads);
+            load_vec<DT, VEC, kHintReduceLoad>(u, i1, tu[q]);
+            load_sign<DT, VEC, kHintReduceLoad, BM>(zs, i1, tz[q]);
+            load_vec<DT, VEC, kHintReduceLoad>(dz, i1, tg[q]);
         }
-        float sdy = 0.f, sdyx = 0.f;
+        float sdy = 0.f, sdyw = 0.f;
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
+        for (int q = 0; q < U; ++q) {
 #pragma unroll
             for (int k = 0; k < VEC; ++k) {
-                float dy, xhat;
-                el(tz[u][k], tg[u][k], dy, xhat);
+                float dy, w;
+                el(tu[q][k], tz[q][k], tg[q][k], dy, w);
                 sdy += dy;
-                sdyx = fmaf(dy, xhat, sdyx);
+                sdyw = fmaf(dy, w, sdyw);
             }
         }
         acc_dy += sdy;
-        acc_dyx += sdyx;
+        acc_dyw += sdyw;
     }
     for (; v < s.hi; v += kThreads) {
-        float tz[VEC], tg[VEC];
+        float tu[VEC], tz[VEC], tg[VEC];
         const uint64_t i1 = access_index(g, cbase, v);
-        load_vec<DT, VEC, kHintReduceLoad>(z, i1, tz);
+        load_vec<DT, VEC, kHintReduceLoad>(u, i1, tu);
+        load_sign<DT, VEC, kHintReduceLoad, BM>(zs, i1, tz);
         load_vec<DT, VEC, kHintReduceLoad>(dz, i1, tg);
-        float sdy = 0.f, sdyx = 0.f;
+        float sdy = 0.f, sdyw = 0.f;
 #pragma unroll
         for (int k = 0; k < VEC; ++k) {
-            float dy, xhat;
-            el(tz[k], tg[k], dy, xhat);
+            float dy, w;
+            el(tu[k], tz[k], tg[k], dy, w);
             sdy += dy;
-            sdyx = fmaf(dy, xhat, sdyx);
+            sdyw = fmaf(dy, w, sdyw);
         }
         acc_dy += sdy;
-        acc_dyx += sdyx;
+        acc_dyw += sdyw;
     }
     acc_dy = wave_sum(acc_dy);
-    acc_dyx = wave_sum(acc_dyx);
+    acc_dyw = wave_sum(acc_dyw);
     if (lane_id() == 0) {
         Partial r;
         r.a = acc_dy;
-        r.b = acc_dyx;
+        r.b = acc_dyw;
         r.c = 0.0;
         r.d = 0.0;
         part[(static_cast<uint64_t>(s.c) * g.P + s.p) * kWaves + threadIdx.x / kWave] = r;
     }
 }
 
-struct BwdParams {
-    const float* gamma;
-    const float* beta;
-    const float* save_var;
-    float* dgamma;
-    float* dbeta;
-    float eps, slope;
-};
-
 // dx = (dy - dgamma*xhat/m - dbeta/m) * gamma/sqrt(var + eps), in place over dz,
-// as dx = A*dy + B*xhat + Cc with per-channel A, B, Cc formed in double.
-template <int DT, int VEC, int U>
-__global__ __launch_bounds__(kThreads) void bwd_apply_kernel(const void* __restrict__ z,
+// with the per-channel constants of make_apply_elem.
+template <int DT, int VEC, int U, int BM>
+__global__ __launch_bounds__(kThreads) void bwd_apply_kernel(const void* __restrict__ u,
+                                                             const void* __restrict__ zs,
                                                              void* __restrict__ dzdx, Geom g,
                                                              const Partial* __restrict__ part,
                                                              BwdParams prm) {
@@ -538,24 +695,26 @@ __global__ __launch_bounds__(kThreads) void bwd_apply_kernel(const void* __restr
     const uint64_t cbase = static_cast<uint64_t>(s.c) * g.vrow;
 
     uint32_t v = s.lo + threadIdx.x;
-    float tz[U][VEC], tg[U][VEC];
+    float tu[U][VEC], tz[U][VEC], tg[U][VEC];
     uint64_t idx[U];
     bool full = v + (U - 1) * kThreads < s.hi;
     if (full) {
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
-            idx[u] = access_index(g, cbase, v + u * kThreads);
-            load_vec<DT, VEC, kHintBwdApplyLoad>(z, idx[u], tz[u]);
-            load_vec<DT, VEC, kHintBwdApplyLoad>(dzdx, idx[u], tg[u]);
+        for (int q = 0; q < U; ++q) {
+            idx[q] = access_index(g, cbase, v + q * kThreads);
+            load_vec<DT, VEC, kHintBwdApplyLoad>(u, idx[q], tu[q]);
+            load_sign<DT, VEC, kHintBwdApplyLoad, BM>(zs, idx[q], tz[q]);
+            load_vec<DT, VEC, kHintBwdApplyLoad>(dzdx, idx[q], tg[q]);
         }
     }
 
     double dbeta, dgamma;
     channel_sums(g, part, s.c, dbeta, dgamma);
-    const double A = static_cast<double>(prm.gamma[s.c]) /
-                     sqrt(static_cast<double>(prm.save_var[s.c]) + static_cast<double>(prm.eps));
-    const BwdApplyElem dx_of =
-        make_apply_elem(A, dgamma, dbeta, g.m, prm.slope, prm.gamma[s.c], prm.beta[s.c]);
+    const double invstd = chan_invstd(prm, s.c);
+    const double A = static_cast<double>(prm.gamma[s.c]) * invstd;
+    const BwdApplyElem<BM> dx_of = make_apply_elem<BM>(
+        A, dgamma, dbeta, g.m, prm.slope, prm.gamma[s.c], prm.beta[s.c],
+        BM == kBwdFromXZ ? prm.save_mean[s.c] : 0.f, invstd, prm.ii != 0);
     if (s.p == 0 && threadIdx.x == 0) {
         prm.dgamma[s.c] = static_cast<float>(dgamma);
         prm.dbeta[s.c] = static_cast<float>(dbeta);
@@ -563,29 +722,31 @@ __global__ __launch_bounds__(kThreads) void bwd_apply_kernel(const void* __restr
 
     while (full) {
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
+        for (int q = 0; q < U; ++q) {
 #pragma unroll
-            for (int k = 0; k < VEC; ++k) tg[u][k] = dx_of(tz[u][k], tg[u][k]);
-            store_vec<DT, VEC, kHintBwdApplyStore>(dzdx, idx[u], tg[u]);
+            for (int k = 0; k < VEC; ++k) tg[q][k] = dx_of(tu[q][k], tz[q][k], tg[q][k]);
+            store_vec<DT, VEC, kHintBwdApplyStore>(dzdx, idx[q], tg[q]);
         }
         v += U * kThreads;
         full = v + (U - 1) * kThreads < s.hi;
         if (full) {
 #pragma unroll
-            for (int u = 0; u < U; ++u) {
-                idx[u] = access_index(g, cbase, v + u * kThreads);
-                load_vec<DT, VEC, kHintBwdApplyLoad>(z, idx[u], tz[u]);
-                load_vec<DT, VEC, kHintBwdApplyLoad>(dzdx, idx[u], tg[u]);
+            for (int q = 0; q < U; ++q) {
+                idx[q] = access_index(g, cbase, v + q * kThreads);
+                load_vec<DT, VEC, kHintBwdApplyLoad>(u, idx[q], tu[q]);
+                load_sign<DT, VEC, kHintBwdApplyLoad, BM>(zs, idx[q], tz[q]);
+                load_vec<DT, VEC, kHintBwdApplyLoad>(dzdx, idx[q], tg[q]);
             }
         }
     }
     for (; v < s.hi; v += kThreads) {
-        float rz[VEC], rg[VEC];
+        float ru[VEC], rz[VEC], rg[VEC];
         const uint64_t i1 = access_index(g, cbase, v);
-        load_vec<DT, VEC, kHintBwdApplyLoad>(z, i1, rz);
+        load_vec<DT, VEC, kHintBwdApplyLoad>(u, i1, ru);
+        load_sign<DT, VEC, kHintBwdApplyLoad, BM>(zs, i1, rz);
         load_vec<DT, VEC, kHintBwdApplyLoad>(dzdx, i1, rg);
 #pragma unroll
-        for (int k = 0; k < VEC; ++k) rg[k] = dx_of(rz[k], rg[k]);
+        for (int k = 0; k < VEC; ++k) rg[k] = dx_of(ru[k], rz[k], rg[k]);
         store_vec<DT, VEC, kHintBwdApplyStore>(dzdx, i1, rg);
     }
 }
@@ -752,14 +913,40 @@ __device__ __forceinline__ float leaky(float y, float a) {
     return SMALL_SLOPE ? fmaxf(y, a * y) : fminf(y, a * y);
 }
 
-// Apply phase of the fused forward: z = f((x - mean_hi) * scale + bshift) for
-// the thread's resident accesses (from registers) and the remainder (loaded
-// again), stored over x.
-template <int DT, int VEC, int T, int R, bool STRIP, bool SMALL_SLOPE>
+// Per-channel constants of the fused forward's apply phase.
+struct FwdApplyK {
+    float mean_hi, scale, bshift, slope;  // y = (x - mean_hi) * scale + bshift (kFwdCkpt: xhat)
+    float gamma, beta;                    // kFwdCkpt: y = gamma * xhat + beta
+    void* out;                            // kFwdOut / kFwdCkpt: z
+};
+
+// The outputs of one 16-byte access from its input values t (overwritten).
+template <int DT, int VEC, int FM, bool SMALL_SLOPE>
+__device__ __forceinline__ void fwd_fused_emit(void* __restrict__ xz, uint64_t idx,
+                                               float (&t)[VEC], const FwdApplyK& k) {
+    if constexpr (FM == kFwdCkpt) {
+        float zv[VEC];
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) {
+            t[e] = storage_round<DT>(fmaf(t[e] - k.mean_hi, k.scale, k.bshift));
+            zv[e] = leaky<SMALL_SLOPE>(fmaf(t[e], k.gamma, k.beta), k.slope);
+        }
+        store_vec<DT, VEC, kHintFwdApplyStore>(xz, idx, t);
+        store_vec<DT, VEC, kHintFwdApplyStore>(k.out, idx, zv);
+    } else {
+#pragma unroll
+        for (int e = 0; e < VEC; ++e)
+            t[e] = leaky<SMALL_SLOPE>(fmaf(t[e] - k.mean_hi, k.scale, k.bshift), k.slope);
+        store_vec<DT, VEC, kHintFwdApplyStore>(FM == kFwdOut ? k.out : xz, idx, t);
+    }
+}
+
+// Apply phase of the fused forward for the thread's resident accesses (from
+// registers) and the remainder (loaded again).
+template <int DT, int VEC, int T, int R, bool STRIP, int FM, bool SMALL_SLOPE>
 __device__ __forceinline__ void fwd_fused_apply(void* __restrict__ xz, const Geom& g, uint32_t c,
                                                 uint32_t tid, const raw16_t (&keep)[R],
-                                                float mean_hi, float scale, float bshift,
-                                                float slope) {
+                                                const FwdApplyK& kk) {
     const uint64_t cbase = static_cast<uint64_t>(c) * g.vrow;
     const uint32_t nstrips = STRIP ? g.vchan / T : 0;
     StripPos sq = strip_begin(g, c);
@@ -779,10 +966,7 @@ __device__ __forceinline__ void fwd_fused_apply(void* __restrict__ xz, const Geo
         if (live) {
             float t[VEC];
             unpack<DT, VEC>(keep[k], t);
-#pragma unroll
-            for (int e = 0; e < VEC; ++e)
-                t[e] = leaky<SMALL_SLOPE>(fmaf(t[e] - mean_hi, scale, bshift), slope);
-            store_vec<DT, VEC, kHintFwdApplyStore>(xz, idx, t);
+            fwd_fused_emit<DT, VEC, FM, SMALL_SLOPE>(xz, idx, t, kk);
         }
         sched_fence();
     }
@@ -792,10 +976,7 @@ __device__ __forceinline__ void fwd_fused_apply(void* __restrict__ xz, const Geo
             const uint64_t idx = sq.off + tid;
             float t[VEC];
             unpack<DT, VEC>(load_raw<kStream>(xz, idx), t);
-#pragma unroll
-            for (int e = 0; e < VEC; ++e)
-                t[e] = leaky<SMALL_SLOPE>(fmaf(t[e] - mean_hi, scale, bshift), slope);
-            store_vec<DT, VEC, kHintFwdApplyStore>(xz, idx, t);
+            fwd_fused_emit<DT, VEC, FM, SMALL_SLOPE>(xz, idx, t, kk);
             strip_next<T>(g, sq);
         }
     } else {
@@ -804,17 +985,14 @@ __device__ __forceinline__ void fwd_fused_apply(void* __restrict__ xz, const Geo
             const uint64_t idx = access_index(g, cbase, v);
             float t[VEC];
             unpack<DT, VEC>(load_raw<kStream>(xz, idx), t);
-#pragma unroll
-            for (int e = 0; e < VEC; ++e)
-                t[e] = leaky<SMALL_SLOPE>(fmaf(t[e] - mean_hi, scale, bshift), slope);
-            store_vec<DT, VEC, kHintFwdApplyStore>(xz, idx, t);
+            fwd_fused_emit<DT, VEC, FM, SMALL_SLOPE>(xz, idx, t, kk);
         }
     }
 }
 
 // Training forward of one channel per block (statistics, running estimates,
 // z over x), same arithmetic as fwd_stats_kernel + fwd_apply_kernel.
-template <int DT, int VEC, int T, int R, bool STRIP>
+template <int DT, int VEC, int T, int R, bool STRIP, int FM>
 __device__ __forceinline__ void fwd_fused_channel(void* __restrict__ xz, const Geom& g,
                                                   const FwdParams& prm, uint32_t c) {
     const uint64_t cbase = static_cast<uint64_t>(c) * g.vrow;
@@ -897,13 +1075,21 @@ __device__ __forceinline__ void fwd_fused_channel(void* __restrict__ xz, const G
     opaque(tid2);
 #pragma unroll
     for (int k = 0; k < R; ++k) opaque(keep[k]);
-    const double scale_d = static_cast<double>(gamma_c) / sqrt(var + static_cast<double>(prm.eps));
+    const double invstd = 1.0 / sqrt(var + static_cast<double>(prm.eps));
+    const double scale_d = FM == kFwdCkpt ? invstd : static_cast<double>(gamma_c) * invstd;
     const float mean_hi = static_cast<float>(mean);
     const double mean_lo = mean - static_cast<double>(mean_hi);
-    const float scale = static_cast<float>(scale_d);
-    // (x - mu) * scale + beta with mu = mean_hi + mean_lo: the low part goes into the shift.
-    const float bshift = static_cast<float>(static_cast<double>(beta_c) - mean_lo * scale_d);
-    const float slope = prm.slope;
+    // (x - mu) * scale + beta with mu = mean_hi + mean_lo: the low part goes
+    // into the shift (kFwdCkpt: beta comes after the rounding of xhat).
+    FwdApplyK kk;
+    kk.mean_hi = mean_hi;
+    kk.scale = static_cast<float>(scale_d);
+    kk.bshift = static_cast<float>((FM == kFwdCkpt ? 0.0 : static_cast<double>(beta_c)) -
+                                   mean_lo * scale_d);
+    kk.slope = prm.slope;
+    kk.gamma = gamma_c;
+    kk.beta = beta_c;
+    kk.out = prm.out;
     if (tid == 0) {
         const double mom = prm.momentum;
         const double m = g.m;
@@ -914,43 +1100,98 @@ __device__ __forceinline__ void fwd_fused_channel(void* __restrict__ xz, const G
                                                 mom * var * (m / (m - 1.0)));
     }
 
-    if (slope <= 1.f)
-        fwd_fused_apply<DT, VEC, T, R, STRIP, true>(xz, g, c, tid2, keep, mean_hi, scale, bshift, slope);
+    if (kk.slope <= 1.f)
+        fwd_fused_apply<DT, VEC, T, R, STRIP, FM, true>(xz, g, c, tid2, keep, kk);
     else
-        fwd_fused_apply<DT, VEC, T, R, STRIP, false>(xz, g, c, tid2, keep, mean_hi, scale, bshift, slope);
+        fwd_fused_apply<DT, VEC, T, R, STRIP, FM, false>(xz, g, c, tid2, keep, kk);
 }
 
-// Backward of one channel per block (sums of dy and dy*xhat, dgamma, dbeta,
-// dx over dz), same arithmetic as bwd_reduce_kernel + bwd_apply_kernel.
-template <int DT, int VEC, int T, int R, bool STRIP>
-__device__ __forceinline__ void bwd_fused_channel(const void* __restrict__ z,
+// Backward of one channel per block (sums of dy and dy*w, dgamma, dbeta, dx
+// over dz), same arithmetic as bwd_reduce_kernel + bwd_apply_kernel.  u is z,
+// x or xhat (see BwdSign).  kBwdFromXZ reads the stored z as well but keeps
+// only its signs (one bit per element) for the apply phase.
+template <int DT, int VEC, int T, int R, bool STRIP, int BM>
+__device__ __forceinline__ void bwd_fused_channel(const void* __restrict__ u,
+                                                  const void* __restrict__ zs,
                                                   void* __restrict__ dzdx, const Geom& g,
                                                   const BwdParams& prm, uint32_t c) {
+    constexpr bool XZ = BM == kBwdFromXZ;
+    constexpr int NW = XZ ? (R * VEC + 31) / 32 : 1;
     const uint64_t cbase = static_cast<uint64_t>(c) * g.vrow;
     const uint32_t tid = threadIdx.x;
     const uint32_t nstrips = STRIP ? g.vchan / T : 0;
-    const raw16_t* const zv = static_cast<const raw16_t*>(z);
+    const raw16_t* const uv = static_cast<const raw16_t*>(u);
+    const raw16_t* const zsv = static_cast<const raw16_t*>(zs);
     const raw16_t* const gv = static_cast<const raw16_t*>(dzdx);
     // All per-channel inputs first: a load issued after the data loads would
     // put another memory round trip after the reduction barrier.
     const float gamma_c = prm.gamma[c], beta_c = prm.beta[c], var_c = prm.save_var[c];
-    const BwdReduceElem el = make_reduce_elem(prm.slope, gamma_c, beta_c);
+    const float mean_c = XZ ? prm.save_mean[c] : 0.f;
+    const double invstd =
+        1.0 / sqrt(static_cast<double>(var_c) + static_cast<double>(prm.eps));
+    const BwdReduceElem<BM> el =
+        make_reduce_elem<BM>(prm.slope, gamma_c, beta_c, mean_c, invstd, prm.ii != 0);
 
     // Register-resident accesses non-temporal, the rest cached (see
-    // fwd_fused_channel).
-    raw16_t kz[R], kg[R];
-    StripPos sp = strip_begin(g, c);
+    // fwd_fused_channel).  kBwdFromXZ first loads z (into the registers x
+    // will use) and dz, turns z into sign bits, and only then loads x, so
+    // that no more than two tensors' worth of registers is live.
+    raw16_t ku[R], kg[R];
+    uint32_t negm[NW];
 #pragma unroll
-    for (int k = 0; k < R; ++k) {
+    for (int q = 0; q < NW; ++q) negm[q] = 0u;
+    auto resident_index = [&](int k, StripPos& p, bool& live) -> uint64_t {
         if constexpr (STRIP) {
-            kz[k] = load_raw<kStream>(zv, sp.off + tid);
-            kg[k] = load_raw<kStream>(gv, sp.off + tid);
-            strip_next<T>(g, sp);
+            const uint64_t i = p.off + tid;
+            strip_next<T>(g, p);
+            live = true;
+            return i;
         } else {
             const uint32_t v = tid + k * T;
-            if (v < g.vchan) {
-                const uint64_t i1 = access_index(g, cbase, v);
-                kz[k] = load_raw<kStream>(z, i1);
+            live = v < g.vchan;
+            return live ? access_index(g, cbase, v) : 0;
+        }
+    };
+    StripPos sp = strip_begin(g, c);
+    if constexpr (XZ) {
+        StripPos sz = sp;
+#pragma unroll
+        for (int k = 0; k < R; ++k) {
+            bool live;
+            const uint64_t i1 = resident_index(k, sz, live);
+            if (live) {
+                ku[k] = load_raw<kStream>(zs, i1);
+                kg[k] = load_raw<kStream>(dzdx, i1);
+            }
+        }
+#pragma unroll
+        for (int k = 0; k < R; ++k) {
+            if (STRIP || tid + k * T < g.vchan) {
+                float tz[VEC];
+                unpack<DT, VEC>(ku[k], tz);
+#pragma unroll
+                for (int e = 0; e < VEC; ++e)
+                    negm[(k * VEC + e) / 32] |= static_cast<uint32_t>(tz[e] < 0.f)
+                                                << ((k * VEC + e) % 32);
+            }
+        }
+        // The bits must exist before the x loads are issued (a memory clobber
+        // keeps the loads below this point and the bit arithmetic above it).
+#pragma unroll
+        for (int q = 0; q < NW; ++q) asm volatile("" : "+v"(negm[q])::"memory");
+#pragma unroll
+        for (int k = 0; k < R; ++k) {
+            bool live;
+            const uint64_t i1 = resident_index(k, sp, live);
+            if (live) ku[k] = load_raw<kStream>(u, i1);
+        }
+    } else {
+#pragma unroll
+        for (int k = 0; k < R; ++k) {
+            bool live;
+            const uint64_t i1 = resident_index(k, sp, live);
+            if (live) {
+                ku[k] = load_raw<kStream>(u, i1);
                 kg[k] = load_raw<kStream>(dzdx, i1);
             }
         }
@@ -958,118 +1199,137 @@ __device__ __forceinline__ void bwd_fused_channel(const void* __restrict__ z,
     // fp32 within one access, fp64 across accesses (as the streaming reduce
     // does per unrolled step): a channel's sums of dy cancel to near zero and
     // an fp32 running sum over the whole register-resident part loses that.
-    double acc_dy = 0.0, acc_dyx = 0.0;
-    float sdy = 0.f, sdyx = 0.f;
-    auto accumulate = [&](raw16_t rz, raw16_t rg) {
-        float tz[VEC], tg[VEC];
-        unpack<DT, VEC>(rz, tz);
-        unpack<DT, VEC>(rg, tg);
-#pragma unroll
-        for (int e = 0; e < VEC; ++e) {
-            float dy, xhat;
-            el(tz[e], tg[e], dy, xhat);
-            sdy += dy;
-            sdyx = fmaf(dy, xhat, sdyx);
-        }
-    };
+    double acc_dy = 0.0, acc_dyw = 0.0;
 #pragma unroll
     for (int k = 0; k < R; ++k) {
         if (STRIP || tid + k * T < g.vchan) {
-            float tz[VEC], tg[VEC];
-            unpack<DT, VEC>(kz[k], tz);
+            float tu[VEC], tg[VEC];
+            unpack<DT, VEC>(ku[k], tu);
             unpack<DT, VEC>(kg[k], tg);
-            sdy = 0.f;
-            sdyx = 0.f;
+            float sdy = 0.f, sdyw = 0.f;
 #pragma unroll
             for (int e = 0; e < VEC; ++e) {
-                float dy, xhat;
-                el(tz[e], tg[e], dy, xhat);
+                float dy, w;
+                if constexpr (XZ) {
+                    const bool neg = (negm[(k * VEC + e) / 32] >> ((k * VEC + e) % 32)) & 1u;
+                    el.with_neg(neg, tu[e], tg[e], dy, w);
+                } else {
+                    el(tu[e], 0.f, tg[e], dy, w);
+                }
                 sdy += dy;
-                sdyx = fmaf(dy, xhat, sdyx);
+                sdyw = fmaf(dy, w, sdyw);
             }
             acc_dy += sdy;
-            acc_dyx += sdyx;
+            acc_dyw += sdyw;
         }
         sched_fence();
     }
+    auto accumulate = [&](uint64_t i1) {
+        float tu[VEC], tz[VEC], tg[VEC];
+        unpack<DT, VEC>(load_raw<kCached>(u, i1), tu);
+        if constexpr (XZ) unpack<DT, VEC>(load_raw<kCached>(zs, i1), tz);
+        else
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) tz[e] = 0.f;
+        unpack<DT, VEC>(load_raw<kCached>(dzdx, i1), tg);
+        float sdy = 0.f, sdyw = 0.f;
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) {
+            float dy, w;
+            el(tu[e], tz[e], tg[e], dy, w);
+            sdy += dy;
+            sdyw = fmaf(dy, w, sdyw);
+        }
+        acc_dy += sdy;
+        acc_dyw += sdyw;
+    };
     if constexpr (STRIP) {
 #pragma unroll 1
         for (uint32_t k = R; k < nstrips; ++k) {
-            sdy = 0.f;
-            sdyx = 0.f;
-            accumulate((zv + sp.off)[tid], (gv + sp.off)[tid]);
-            acc_dy += sdy;
-            acc_dyx += sdyx;
+            accumulate(sp.off + tid);
             strip_next<T>(g, sp);
         }
     } else {
 #pragma unroll 1
-        for (uint32_t v = tid + R * T; v < g.vchan; v += T) {
-            const uint64_t i1 = access_index(g, cbase, v);
-            sdy = 0.f;
-            sdyx = 0.f;
-            accumulate(load_raw<kCached>(z, i1), load_raw<kCached>(dzdx, i1));
-            acc_dy += sdy;
-            acc_dyx += sdyx;
-        }
+        for (uint32_t v = tid + R * T; v < g.vchan; v += T) accumulate(access_index(g, cbase, v));
     }
 
-    double dbeta, dgamma;
-    block_sums<T>(acc_dy, acc_dyx, dbeta, dgamma);
+    double dbeta, sdyw;
+    block_sums<T>(acc_dy, acc_dyw, dbeta, sdyw);
     uint32_t tid2 = tid;
     opaque(tid2);
 #pragma unroll
     for (int k = 0; k < R; ++k) {
-        opaque(kz[k]);
+        opaque(ku[k]);
         opaque(kg[k]);
     }
-    const double A = static_cast<double>(gamma_c) /
-                     sqrt(static_cast<double>(var_c) + static_cast<double>(prm.eps));
-    const BwdApplyElem dx_of = make_apply_elem(A, dgamma, dbeta, g.m, prm.slope, gamma_c, beta_c);
+#pragma unroll
+    for (int q = 0; q < NW; ++q) opaque(negm[q]);
+    const double A = static_cast<double>(gamma_c) * invstd;
+    const BwdApplyElem<BM> dx_of = make_apply_elem<BM>(A, sdyw, dbeta, g.m, prm.slope, gamma_c,
+                                                       beta_c, mean_c, invstd, prm.ii != 0);
     if (tid == 0) {
-        prm.dgamma[c] = static_cast<float>(dgamma);
+        prm.dgamma[c] = static_cast<float>(sdyw);
         prm.dbeta[c] = static_cast<float>(dbeta);
     }
-    auto emit = [&](raw16_t rz, raw16_t rg, uint64_t idx) {
-        float tz[VEC], tg[VEC];
-        unpack<DT, VEC>(rz, tz);
+    auto emit = [&](raw16_t ru, raw16_t rz, raw16_t rg, uint64_t idx) {
+        float tu[VEC], tz[VEC], tg[VEC];
+        unpack<DT, VEC>(ru, tu);
+        if constexpr (XZ) unpack<DT, VEC>(rz, tz);
+        else
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) tz[e] = 0.f;
         unpack<DT, VEC>(rg, tg);
 #pragma unroll
-        for (int e = 0; e < VEC; ++e) tg[e] = dx_of(tz[e], tg[e]);
+        for (int e = 0; e < VEC; ++e) tg[e] = dx_of(tu[e], tz[e], tg[e]);
         store_vec<DT, VEC, kHintBwdApplyStore>(dzdx, idx, tg);
     };
+    // The resident accesses: dx from registers (kBwdFromXZ: signs from the bits).
     StripPos sq = strip_begin(g, c);
 #pragma unroll
     for (int k = 0; k < R; ++k) {
+        uint64_t idx = 0;
+        bool live = true;
         if constexpr (STRIP) {
-            emit(kz[k], kg[k], sq.off + tid2);
+            idx = sq.off + tid2;
             strip_next<T>(g, sq);
         } else {
             const uint32_t v = tid2 + k * T;
-            if (v < g.vchan) {
-                const uint64_t i1 = access_index(g, cbase, v);
-                float tz[VEC], tg[VEC];
-                unpack<DT, VEC>(kz[k], tz);
-                unpack<DT, VEC>(kg[k], tg);
+            live = v < g.vchan;
+            if (live) idx = access_index(g, cbase, v);
+        }
+        if (live) {
+            float tu[VEC], tg[VEC];
+            unpack<DT, VEC>(ku[k], tu);
+            unpack<DT, VEC>(kg[k], tg);
 #pragma unroll
-                for (int e = 0; e < VEC; ++e) tg[e] = dx_of(tz[e], tg[e]);
-                store_vec<DT, VEC, kHintBwdApplyStore>(dzdx, i1, tg);
+            for (int e = 0; e < VEC; ++e) {
+                if constexpr (XZ) {
+                    const bool neg = (negm[(k * VEC + e) / 32] >> ((k * VEC + e) % 32)) & 1u;
+                    tg[e] = dx_of.with_neg(neg, tu[e], tg[e]);
+                } else {
+                    tg[e] = dx_of(tu[e], 0.f, tg[e]);
+                }
             }
+            store_vec<DT, VEC, kHintBwdApplyStore>(dzdx, idx, tg);
         }
         sched_fence();
     }
+    const raw16_t zero16 = {0u, 0u, 0u, 0u};
     if constexpr (STRIP) {
 #pragma unroll 1
         for (uint32_t k = R; k < nstrips; ++k) {
             const uint64_t i1 = sq.off + tid2;
-            emit(load_raw<kStream>(z, i1), load_raw<kStream>(dzdx, i1), i1);
+            emit(load_raw<kStream>(u, i1), XZ ? load_raw<kStream>(zs, i1) : zero16,
+                 load_raw<kStream>(dzdx, i1), i1);
             strip_next<T>(g, sq);
         }
     } else {
 #pragma unroll 1
         for (uint32_t v = tid2 + R * T; v < g.vchan; v += T) {
             const uint64_t i1 = access_index(g, cbase, v);
-            emit(load_raw<kStream>(z, i1), load_raw<kStream>(dzdx, i1), i1);
+            emit(load_raw<kStream>(u, i1), XZ ? load_raw<kStream>(zs, i1) : zero16,
+                 load_raw<kStream>(dzdx, i1), i1);
         }
     }
 }
@@ -1083,17 +1343,18 @@ __device__ __forceinline__ void bwd_fused_channel(const void* __restrict__ z,
 // one block, and at that occupancy the per-channel reduce-barrier-apply chain
 // costs more than the overlap of one channel's stores with the next one's
 // loads gains.)
-template <int DT, int VEC, int T, int R, bool STRIP>
+template <int DT, int VEC, int T, int R, bool STRIP, int FM>
 __global__ __launch_bounds__(T) void fwd_fused_kernel(void* __restrict__ xz, Geom g,
                                                       FwdParams prm) {
-    fwd_fused_channel<DT, VEC, T, R, STRIP>(xz, g, prm, blockIdx.x);
+    fwd_fused_channel<DT, VEC, T, R, STRIP, FM>(xz, g, prm, blockIdx.x);
 }
 
-template <int DT, int VEC, int T, int R, bool STRIP>
-__global__ __launch_bounds__(T) void bwd_fused_kernel(const void* __restrict__ z,
+template <int DT, int VEC, int T, int R, bool STRIP, int BM>
+__global__ __launch_bounds__(T) void bwd_fused_kernel(const void* __restrict__ u,
+                                                      const void* __restrict__ zs,
                                                       void* __restrict__ dzdx, Geom g,
                                                       BwdParams prm) {
-    bwd_fused_channel<DT, VEC, T, R, STRIP>(z, dzdx, g, prm, blockIdx.x);
+    bwd_fused_channel<DT, VEC, T, R, STRIP, BM>(u, zs, dzdx, g, prm, blockIdx.x);
 }
 
 // ---------------------------------------------------------------- host side
@@ -1251,34 +1512,59 @@ struct LaunchFwdStats {
     }
 };
 
+// train = false is inference (in place); otherwise fm is the output mode.
 template <int DT, int VEC>
 struct LaunchFwdApply {
     static void run(void* xz, const Geom& g, const Partial* part, const FwdParams& prm, bool train,
-                    hipStream_t st) {
-        if (train)
-            fwd_apply_kernel<DT, VEC, unroll<VEC>(), true><<<grid_of(g), kThreads, 0, st>>>(
-                xz, g, part, prm);
+                    int fm, hipStream_t st) {
+        constexpr int U = unroll<VEC>();
+        const dim3 grid = grid_of(g);
+        if (!train)
+            fwd_apply_kernel<DT, VEC, U, false, kFwdInPlace><<<grid, kThreads, 0, st>>>(xz, g, part, prm);
+        else if (fm == kFwdOut)
+            fwd_apply_kernel<DT, VEC, U, true, kFwdOut><<<grid, kThreads, 0, st>>>(xz, g, part, prm);
+        else if (fm == kFwdCkpt)
+            fwd_apply_kernel<DT, VEC, U, true, kFwdCkpt><<<grid, kThreads, 0, st>>>(xz, g, part, prm);
         else
-            fwd_apply_kernel<DT, VEC, unroll<VEC>(), false><<<grid_of(g), kThreads, 0, st>>>(
-                xz, g, part, prm);
+            fwd_apply_kernel<DT, VEC, U, true, kFwdInPlace><<<grid, kThreads, 0, st>>>(xz, g, part, prm);
     }
 };
 
 template <int DT, int VEC>
 struct LaunchBwdReduce {
-    static void run(const void* z, const void* dz, const Geom& g, const float* gamma,
-                    const float* beta, float slope, Partial* part, hipStream_t st) {
-        bwd_reduce_kernel<DT, VEC, unroll<VEC>()><<<grid_of(g), kThreads, 0, st>>>(
-            z, dz, g, gamma, beta, slope, part);
+    static void run(const void* u, const void* zs, const void* dz, const Geom& g,
+                    const BwdParams& prm, int bm, Partial* part, hipStream_t st) {
+        constexpr int U = unroll<VEC>();
+        const dim3 grid = grid_of(g);
+        if (bm == kBwdFromXZ)
+            bwd_reduce_kernel<DT, VEC, U, kBwdFromXZ><<<grid, kThreads, 0, st>>>(u, zs, dz, g, prm, part);
+        else if (bm == kBwdFromXhat)
+            bwd_reduce_kernel<DT, VEC, U, kBwdFromXhat><<<grid, kThreads, 0, st>>>(u, zs, dz, g, prm, part);
+        else
+            bwd_reduce_kernel<DT, VEC, U, kBwdFromZ><<<grid, kThreads, 0, st>>>(u, zs, dz, g, prm, part);
     }
 };
 
 template <int DT, int VEC>
 struct LaunchBwdApply {
-    static void run(const void* z, void* dzdx, const Geom& g, const Partial* part,
-                    const BwdParams& prm, hipStream_t st) {
-        bwd_apply_kernel<DT, VEC, unroll<VEC>()><<<grid_of(g), kThreads, 0, st>>>(z, dzdx, g,
-                                                                                   part, prm);
+    static void run(const void* u, const void* zs, void* dzdx, const Geom& g, const Partial* part,
+                    const BwdParams& prm, int bm, hipStream_t st) {
+        constexpr int U = unroll<VEC>();
+        const dim3 grid = grid_of(g);
+        if (bm == kBwdFromXZ)
+            bwd_apply_kernel<DT, VEC, U, kBwdFromXZ><<<grid, kThreads, 0, st>>>(u, zs, dzdx, g, part, prm);
+        else if (bm == kBwdFromXhat)
+            bwd_apply_kernel<DT, VEC, U, kBwdFromXhat><<<grid, kThreads, 0, st>>>(u, zs, dzdx, g, part, prm);
+        else
+            bwd_apply_kernel<DT, VEC, U, kBwdFromZ><<<grid, kThreads, 0, st>>>(u, zs, dzdx, g, part, prm);
+    }
+};
+
+template <int DT, int VEC>
+struct LaunchRecompute {
+    static void run(const void* xhat, void* z, const Geom& g, const float* gamma, const float* beta,
+                    float slope, hipStream_t st) {
+        recompute_kernel<DT, VEC><<<grid_of(g), kThreads, 0, st>>>(xhat, z, g, gamma, beta, slope);
     }
 };
 
@@ -1334,44 +1620,60 @@ bool plan_fused(int64_t C, const Geom& g, bool vector, bool backward, FusedPlan*
     return false;
 }
 
-#define IABN_FUSED_CASE(KERNEL, TT, RR, ...)                                                   \
+#define IABN_FUSED_CASE(KERNEL, MODE, TT, RR, ...)                                             \
     if (fp.T == TT && fp.R == RR) {                                                           \
         if (kUseStrips && g.vrow % TT == 0 && g.vchan / TT >= RR)                             \
-            KERNEL<DT, V, TT, RR, true><<<grid, TT, lds, st>>>(__VA_ARGS__);                  \
+            KERNEL<DT, V, TT, RR, true, MODE><<<grid, TT, lds, st>>>(__VA_ARGS__);            \
         else                                                                                  \
-            KERNEL<DT, V, TT, RR, false><<<grid, TT, lds, st>>>(__VA_ARGS__);                 \
+            KERNEL<DT, V, TT, RR, false, MODE><<<grid, TT, lds, st>>>(__VA_ARGS__);           \
         return true;                                                                          \
     }
 
-template <int DT>
+template <int DT, int FM>
 bool launch_fwd_fused(void* xz, const Geom& g, const FusedPlan& fp, const FwdParams& prm,
                       hipStream_t st) {
     constexpr int V = 16 / sizeof(typename Elem<DT>::T);
     const dim3 grid = fused_grid(g, fp);
     const size_t lds = fused_lds(kFusedFwdBlocksPerCU);
-    IABN_FUSED_CASE(fwd_fused_kernel, 256, 4, xz, g, prm)
-    IABN_FUSED_CASE(fwd_fused_kernel, 512, 4, xz, g, prm)
-    IABN_FUSED_CASE(fwd_fused_kernel, 256, 16, xz, g, prm)
-    IABN_FUSED_CASE(fwd_fused_kernel, 512, 16, xz, g, prm)
-    IABN_FUSED_CASE(fwd_fused_kernel, 1024, 16, xz, g, prm)
+    IABN_FUSED_CASE(fwd_fused_kernel, FM, 256, 4, xz, g, prm)
+    IABN_FUSED_CASE(fwd_fused_kernel, FM, 512, 4, xz, g, prm)
+    IABN_FUSED_CASE(fwd_fused_kernel, FM, 256, 16, xz, g, prm)
+    IABN_FUSED_CASE(fwd_fused_kernel, FM, 512, 16, xz, g, prm)
+    IABN_FUSED_CASE(fwd_fused_kernel, FM, 1024, 16, xz, g, prm)
     return false;
 }
 
-template <int DT>
-bool launch_bwd_fused(const void* z, void* dzdx, const Geom& g, const FusedPlan& fp,
-                      const BwdParams& prm, hipStream_t st) {
+template <int DT, int BM>
+bool launch_bwd_fused(const void* u, const void* zs, void* dzdx, const Geom& g,
+                      const FusedPlan& fp, const BwdParams& prm, hipStream_t st) {
     constexpr int V = 16 / sizeof(typename Elem<DT>::T);
     const dim3 grid = fused_grid(g, fp);
     const size_t lds = fused_lds(kFusedBwdBlocksPerCU);
-    IABN_FUSED_CASE(bwd_fused_kernel, 256, 4, z, dzdx, g, prm)
-    IABN_FUSED_CASE(bwd_fused_kernel, 512, 4, z, dzdx, g, prm)
-    IABN_FUSED_CASE(bwd_fused_kernel, 256, 16, z, dzdx, g, prm)
-    IABN_FUSED_CASE(bwd_fused_kernel, 512, 16, z, dzdx, g, prm)
-    IABN_FUSED_CASE(bwd_fused_kernel, 1024, 8, z, dzdx, g, prm)
+    IABN_FUSED_CASE(bwd_fused_kernel, BM, 256, 4, u, zs, dzdx, g, prm)
+    IABN_FUSED_CASE(bwd_fused_kernel, BM, 512, 4, u, zs, dzdx, g, prm)
+    IABN_FUSED_CASE(bwd_fused_kernel, BM, 256, 16, u, zs, dzdx, g, prm)
+    IABN_FUSED_CASE(bwd_fused_kernel, BM, 512, 16, u, zs, dzdx, g, prm)
+    IABN_FUSED_CASE(bwd_fused_kernel, BM, 1024, 8, u, zs, dzdx, g, prm)
     return false;
 }
 
 #undef IABN_FUSED_CASE
+
+template <int FM>
+bool launch_fwd_fused_dt(int dtype, void* xz, const Geom& g, const FusedPlan& fp,
+                         const FwdParams& prm, hipStream_t st) {
+    return dtype == IABN_F32   ? launch_fwd_fused<IABN_F32, FM>(xz, g, fp, prm, st)
+           : dtype == IABN_F16 ? launch_fwd_fused<IABN_F16, FM>(xz, g, fp, prm, st)
+                               : launch_fwd_fused<IABN_BF16, FM>(xz, g, fp, prm, st);
+}
+
+template <int BM>
+bool launch_bwd_fused_dt(int dtype, const void* u, const void* zs, void* dzdx, const Geom& g,
+                         const FusedPlan& fp, const BwdParams& prm, hipStream_t st) {
+    return dtype == IABN_F32   ? launch_bwd_fused<IABN_F32, BM>(u, zs, dzdx, g, fp, prm, st)
+           : dtype == IABN_F16 ? launch_bwd_fused<IABN_F16, BM>(u, zs, dzdx, g, fp, prm, st)
+                               : launch_bwd_fused<IABN_BF16, BM>(u, zs, dzdx, g, fp, prm, st);
+}
 
 // ---- end fused planning
 
@@ -1381,6 +1683,97 @@ int validate_common(int dtype, int64_t N, int64_t C, int64_t HW, bool train) {
 }
 
 bool empty(int64_t N, int64_t C, int64_t HW) { return C == 0 || N * HW == 0; }
+
+bool vector_ok(int64_t HW, int dtype, const void* a, const void* b, const void* c) {
+    return use_vector(HW, dtype, a, b) && (c == nullptr || aligned16(c));
+}
+
+const char* fwd_name(int fm) {
+    return fm == kFwdOut ? "standard forward" : fm == kFwdCkpt ? "checkpointing forward" : "forward";
+}
+
+// Training forward of the three arms (fm: kFwdInPlace, kFwdOut, kFwdCkpt).
+// x is the input (kFwdInPlace: z on return; kFwdCkpt: xhat on return); out
+// receives z for kFwdOut and kFwdCkpt.  Everything is validated before the
+// first launch, so an error changes nothing.
+int forward_train_impl(int fm, void* x, void* out, int dtype, const float* gamma,
+                       const float* beta, float* running_mean, float* running_var,
+                       float* save_mean, float* save_var, float eps, float momentum, float slope,
+                       int64_t N, int64_t C, int64_t HW, void* workspace, size_t workspace_bytes,
+                       void* stream) {
+    int rc = validate_common(dtype, N, C, HW, true);
+    if (rc) return rc;
+    if (empty(N, C, HW)) return ok();
+    if (!x || !gamma || !beta || !running_mean || !running_var || !save_mean || !save_var ||
+        (fm != kFwdInPlace && !out))
+        return fail(IABN_ERR_NULL, "a tensor or parameter pointer is NULL");
+    if ((rc = check_params(eps, slope))) return rc;
+    if (!(momentum >= 0.f && momentum <= 1.f))
+        return fail(IABN_ERR_PARAM, "momentum must lie in [0, 1]");
+    if ((rc = check_workspace(N, C, HW, workspace, workspace_bytes))) return rc;
+    const bool vec = use_vector(HW, dtype, x, fm == kFwdInPlace ? nullptr : out);
+    const Geom g = make_geom(N, C, HW, dtype, vec);
+    const FwdParams prm = {gamma,    beta, running_mean, running_var, save_mean, save_var,
+                           fm == kFwdInPlace ? nullptr : out, eps, momentum, slope};
+    const hipStream_t st = static_cast<hipStream_t>(stream);
+    FusedPlan fp;
+    if (plan_fused(C, g, vec, false, &fp)) {
+        const bool ok = fm == kFwdOut    ? launch_fwd_fused_dt<kFwdOut>(dtype, x, g, fp, prm, st)
+                        : fm == kFwdCkpt ? launch_fwd_fused_dt<kFwdCkpt>(dtype, x, g, fp, prm, st)
+                                         : launch_fwd_fused_dt<kFwdInPlace>(dtype, x, g, fp, prm, st);
+        if (!ok)
+            return fail(IABN_ERR_HIP, "no %s kernel built for T=%d R=%d", fwd_name(fm), fp.T, fp.R);
+        return launched(fwd_name(fm));
+    }
+    Partial* part = static_cast<Partial*>(workspace);
+    dispatch<LaunchFwdStats>(dtype, vec, static_cast<const void*>(x), g, part, st);
+    if ((rc = launched("fwd_stats"))) return rc;
+    dispatch<LaunchFwdApply>(dtype, vec, x, g, static_cast<const Partial*>(part), prm, true, fm, st);
+    return launched(fwd_name(fm));
+}
+
+const char* bwd_name(int bm, bool ii) {
+    return bm == kBwdFromXZ     ? "standard backward"
+           : bm == kBwdFromXhat ? "checkpointing backward"
+           : ii                 ? "backward (formulation II)"
+                                : "backward";
+}
+
+// Backward of every formulation (bm, ii: see BwdSign).  u is z, x or xhat;
+// zs is the stored z for kBwdFromXZ; dz_dx holds dz on entry, dx on return.
+int backward_impl(int bm, bool ii, const void* u, const void* zs, void* dz_dx, int dtype,
+                  const float* gamma, const float* beta, const float* save_mean,
+                  const float* save_var, float* dgamma, float* dbeta, float eps, float slope,
+                  int64_t N, int64_t C, int64_t HW, void* workspace, size_t workspace_bytes,
+                  void* stream) {
+    int rc = validate_common(dtype, N, C, HW, true);
+    if (rc) return rc;
+    if (empty(N, C, HW)) return ok();
+    if (!u || !dz_dx || !gamma || !beta || !save_var || !dgamma || !dbeta ||
+        (bm == kBwdFromXZ && (!zs || !save_mean)))
+        return fail(IABN_ERR_NULL, "a tensor or parameter pointer is NULL");
+    if ((rc = check_params(eps, slope))) return rc;
+    if ((rc = check_workspace(N, C, HW, workspace, workspace_bytes))) return rc;
+    const bool vec = vector_ok(HW, dtype, u, dz_dx, bm == kBwdFromXZ ? zs : nullptr);
+    const Geom g = make_geom(N, C, HW, dtype, vec);
+    const BwdParams prm = {gamma, beta, save_mean, save_var, dgamma, dbeta, eps, slope, ii ? 1 : 0};
+    const hipStream_t st = static_cast<hipStream_t>(stream);
+    FusedPlan fp;
+    if (plan_fused(C, g, vec, true, &fp)) {
+        const bool ok =
+            bm == kBwdFromXZ     ? launch_bwd_fused_dt<kBwdFromXZ>(dtype, u, zs, dz_dx, g, fp, prm, st)
+            : bm == kBwdFromXhat ? launch_bwd_fused_dt<kBwdFromXhat>(dtype, u, zs, dz_dx, g, fp, prm, st)
+                                 : launch_bwd_fused_dt<kBwdFromZ>(dtype, u, zs, dz_dx, g, fp, prm, st);
+        if (!ok)
+            return fail(IABN_ERR_HIP, "no %s kernel built for T=%d R=%d", bwd_name(bm, ii), fp.T, fp.R);
+        return launched(bwd_name(bm, ii));
+    }
+    Partial* part = static_cast<Partial*>(workspace);
+    dispatch<LaunchBwdReduce>(dtype, vec, u, zs, static_cast<const void*>(dz_dx), g, prm, bm, part, st);
+    if ((rc = launched("bwd_reduce"))) return rc;
+    dispatch<LaunchBwdApply>(dtype, vec, u, zs, dz_dx, g, static_cast<const Partial*>(part), prm, bm, st);
+    return launched(bwd_name(bm, ii));
+}
 
 }  // namespace
 
@@ -1442,9 +1835,9 @@ int iabn_forward_apply(void* x_z, int dtype, const float* gamma, const float* be
     const bool vec = use_vector(HW, dtype, x_z, nullptr);
     const Geom g = make_geom(N, C, HW, dtype, vec);
     const FwdParams prm = {gamma, beta, running_mean, running_var, save_mean, save_var,
-                           eps,   momentum, slope};
+                           nullptr, eps, momentum, slope};
     dispatch<LaunchFwdApply>(dtype, vec, x_z, g, static_cast<const Partial*>(workspace), prm, true,
-                             static_cast<hipStream_t>(stream));
+                             kFwdInPlace, static_cast<hipStream_t>(stream));
     return launched("fwd_apply");
 }
 
@@ -1453,34 +1846,9 @@ int iabn_forward_train(void* x_z, int dtype, const float* gamma, const float* be
                        float* save_var, float eps, float momentum, float slope, int64_t N,
                        int64_t C, int64_t HW, void* workspace, size_t workspace_bytes,
                        void* stream) {
-    // Validate everything before the first launch so that an error changes nothing.
-    int rc = validate_common(dtype, N, C, HW, true);
-    if (rc) return rc;
-    if (empty(N, C, HW)) return ok();
-    if (!x_z || !gamma || !beta || !running_mean || !running_var || !save_mean || !save_var)
-        return fail(IABN_ERR_NULL, "a tensor or parameter pointer is NULL");
-    if ((rc = check_params(eps, slope))) return rc;
-    if (!(momentum >= 0.f && momentum <= 1.f))
-        return fail(IABN_ERR_PARAM, "momentum must lie in [0, 1]");
-    if ((rc = check_workspace(N, C, HW, workspace, workspace_bytes))) return rc;
-    const bool vec = use_vector(HW, dtype, x_z, nullptr);
-    const Geom g = make_geom(N, C, HW, dtype, vec);
-    FusedPlan fp;
-    if (plan_fused(C, g, vec, false, &fp)) {
-        const FwdParams prm = {gamma, beta, running_mean, running_var, save_mean, save_var,
-                               eps,   momentum, slope};
-        const hipStream_t st = static_cast<hipStream_t>(stream);
-        const bool ok = dtype == IABN_F32   ? launch_fwd_fused<IABN_F32>(x_z, g, fp, prm, st)
-                        : dtype == IABN_F16 ? launch_fwd_fused<IABN_F16>(x_z, g, fp, prm, st)
-                                            : launch_fwd_fused<IABN_BF16>(x_z, g, fp, prm, st);
-        if (!ok) return fail(IABN_ERR_HIP, "no forward kernel built for T=%d R=%d", fp.T, fp.R);
-        return launched("fwd_fused");
-    }
-    if ((rc = iabn_forward_stats(x_z, dtype, N, C, HW, workspace, workspace_bytes, stream)))
-        return rc;
-    return iabn_forward_apply(x_z, dtype, gamma, beta, running_mean, running_var, save_mean,
-                              save_var, eps, momentum, slope, N, C, HW, workspace,
-                              workspace_bytes, stream);
+    return forward_train_impl(kFwdInPlace, x_z, nullptr, dtype, gamma, beta, running_mean,
+                              running_var, save_mean, save_var, eps, momentum, slope, N, C, HW,
+                              workspace, workspace_bytes, stream);
 }
 
 int iabn_forward_eval(void* x_z, int dtype, const float* gamma, const float* beta,
@@ -1495,9 +1863,10 @@ int iabn_forward_eval(void* x_z, int dtype, const float* gamma, const float* bet
     const bool vec = use_vector(HW, dtype, x_z, nullptr);
     const Geom g = make_geom(N, C, HW, dtype, vec);
     const FwdParams prm = {gamma, beta, const_cast<float*>(running_mean),
-                           const_cast<float*>(running_var), nullptr, nullptr, eps, 0.f, slope};
+                           const_cast<float*>(running_var), nullptr, nullptr, nullptr, eps, 0.f,
+                           slope};
     dispatch<LaunchFwdApply>(dtype, vec, x_z, g, static_cast<const Partial*>(nullptr), prm, false,
-                             static_cast<hipStream_t>(stream));
+                             kFwdInPlace, static_cast<hipStream_t>(stream));
     return launched("fwd_eval");
 }
 
@@ -1514,8 +1883,10 @@ int iabn_backward_reduce(const void* z, const void* dz, int dtype, const float* 
     if ((rc = check_workspace(N, C, HW, workspace, workspace_bytes))) return rc;
     const bool vec = use_vector(HW, dtype, z, dz);
     const Geom g = make_geom(N, C, HW, dtype, vec);
-    dispatch<LaunchBwdReduce>(dtype, vec, z, dz, g, gamma, beta, slope,
-                              static_cast<Partial*>(workspace), static_cast<hipStream_t>(stream));
+    const BwdParams prm = {gamma, beta, nullptr, nullptr, nullptr, nullptr, 1.f, slope, 0};
+    dispatch<LaunchBwdReduce>(dtype, vec, z, static_cast<const void*>(nullptr), dz, g, prm,
+                              kBwdFromZ, static_cast<Partial*>(workspace),
+                              static_cast<hipStream_t>(stream));
     return launched("bwd_reduce");
 }
 
@@ -1532,8 +1903,9 @@ int iabn_backward_apply(const void* z, void* dz_dx, int dtype, const float* gamm
     if ((rc = check_workspace(N, C, HW, workspace, workspace_bytes))) return rc;
     const bool vec = use_vector(HW, dtype, z, dz_dx);
     const Geom g = make_geom(N, C, HW, dtype, vec);
-    const BwdParams prm = {gamma, beta, save_var, dgamma, dbeta, eps, slope};
-    dispatch<LaunchBwdApply>(dtype, vec, z, dz_dx, g, static_cast<const Partial*>(workspace), prm,
+    const BwdParams prm = {gamma, beta, nullptr, save_var, dgamma, dbeta, eps, slope, 0};
+    dispatch<LaunchBwdApply>(dtype, vec, z, static_cast<const void*>(nullptr), dz_dx, g,
+                             static_cast<const Partial*>(workspace), prm, kBwdFromZ,
                              static_cast<hipStream_t>(stream));
     return launched("bwd_apply");
 }
@@ -1542,30 +1914,71 @@ int iabn_backward(const void* z, void* dz_dx, int dtype, const float* gamma, con
                   const float* save_var, float* dgamma, float* dbeta, float eps, float slope,
                   int64_t N, int64_t C, int64_t HW, void* workspace, size_t workspace_bytes,
                   void* stream) {
-    int rc = validate_common(dtype, N, C, HW, true);
+    return backward_impl(kBwdFromZ, false, z, nullptr, dz_dx, dtype, gamma, beta, nullptr,
+                         save_var, dgamma, dbeta, eps, slope, N, C, HW, workspace,
+                         workspace_bytes, stream);
+}
+
+int iabn_backward_ii(const void* z, void* dz_dx, int dtype, const float* gamma,
+                     const float* beta, const float* save_var, float* dgamma, float* dbeta,
+                     float eps, float slope, int64_t N, int64_t C, int64_t HW, void* workspace,
+                     size_t workspace_bytes, void* stream) {
+    return backward_impl(kBwdFromZ, true, z, nullptr, dz_dx, dtype, gamma, beta, nullptr,
+                         save_var, dgamma, dbeta, eps, slope, N, C, HW, workspace,
+                         workspace_bytes, stream);
+}
+
+int iabn_std_forward_train(const void* x, void* z, int dtype, const float* gamma,
+                           const float* beta, float* running_mean, float* running_var,
+                           float* save_mean, float* save_var, float eps, float momentum,
+                           float slope, int64_t N, int64_t C, int64_t HW, void* workspace,
+                           size_t workspace_bytes, void* stream) {
+    return forward_train_impl(kFwdOut, const_cast<void*>(x), z, dtype, gamma, beta, running_mean,
+                              running_var, save_mean, save_var, eps, momentum, slope, N, C, HW,
+                              workspace, workspace_bytes, stream);
+}
+
+int iabn_std_backward(const void* x, const void* z, void* dz_dx, int dtype, const float* gamma,
+                      const float* beta, const float* save_mean, const float* save_var,
+                      float* dgamma, float* dbeta, float eps, float slope, int64_t N, int64_t C,
+                      int64_t HW, void* workspace, size_t workspace_bytes, void* stream) {
+    return backward_impl(kBwdFromXZ, false, x, z, dz_dx, dtype, gamma, beta, save_mean, save_var,
+                         dgamma, dbeta, eps, slope, N, C, HW, workspace, workspace_bytes, stream);
+}
+
+int iabn_ckpt_forward_train(void* x_xhat, void* z, int dtype, const float* gamma,
+                            const float* beta, float* running_mean, float* running_var,
+                            float* save_mean, float* save_var, float eps, float momentum,
+                            float slope, int64_t N, int64_t C, int64_t HW, void* workspace,
+                            size_t workspace_bytes, void* stream) {
+    return forward_train_impl(kFwdCkpt, x_xhat, z, dtype, gamma, beta, running_mean, running_var,
+                              save_mean, save_var, eps, momentum, slope, N, C, HW, workspace,
+                              workspace_bytes, stream);
+}
+
+int iabn_ckpt_recompute(const void* xhat, void* z, int dtype, const float* gamma,
+                        const float* beta, float slope, int64_t N, int64_t C, int64_t HW,
+                        void* stream) {
+    int rc = validate_common(dtype, N, C, HW, false);
     if (rc) return rc;
     if (empty(N, C, HW)) return ok();
-    if (!z || !dz_dx || !gamma || !beta || !save_var || !dgamma || !dbeta)
+    if (!xhat || !z || !gamma || !beta)
         return fail(IABN_ERR_NULL, "a tensor or parameter pointer is NULL");
-    if ((rc = check_params(eps, slope))) return rc;
-    if ((rc = check_workspace(N, C, HW, workspace, workspace_bytes))) return rc;
-    const bool vec = use_vector(HW, dtype, z, dz_dx);
+    if ((rc = check_params(1.f, slope))) return rc;
+    const bool vec = use_vector(HW, dtype, xhat, z);
     const Geom g = make_geom(N, C, HW, dtype, vec);
-    FusedPlan fp;
-    if (plan_fused(C, g, vec, true, &fp)) {
-        const BwdParams prm = {gamma, beta, save_var, dgamma, dbeta, eps, slope};
-        const hipStream_t st = static_cast<hipStream_t>(stream);
-        const bool ok = dtype == IABN_F32   ? launch_bwd_fused<IABN_F32>(z, dz_dx, g, fp, prm, st)
-                        : dtype == IABN_F16 ? launch_bwd_fused<IABN_F16>(z, dz_dx, g, fp, prm, st)
-                                            : launch_bwd_fused<IABN_BF16>(z, dz_dx, g, fp, prm, st);
-        if (!ok) return fail(IABN_ERR_HIP, "no backward kernel built for T=%d R=%d", fp.T, fp.R);
-        return launched("bwd_fused");
-    }
-    if ((rc = iabn_backward_reduce(z, dz_dx, dtype, gamma, beta, slope, N, C, HW, workspace,
-                                   workspace_bytes, stream)))
-        return rc;
-    return iabn_backward_apply(z, dz_dx, dtype, gamma, beta, save_var, dgamma, dbeta, eps, slope,
-                               N, C, HW, workspace, workspace_bytes, stream);
+    dispatch<LaunchRecompute>(dtype, vec, xhat, z, g, gamma, beta, slope,
+                              static_cast<hipStream_t>(stream));
+    return launched("recompute");
+}
+
+int iabn_ckpt_backward(const void* xhat, void* dz_dx, int dtype, const float* gamma,
+                       const float* beta, const float* save_var, float* dgamma, float* dbeta,
+                       float eps, float slope, int64_t N, int64_t C, int64_t HW,
+                       void* workspace, size_t workspace_bytes, void* stream) {
+    return backward_impl(kBwdFromXhat, false, xhat, nullptr, dz_dx, dtype, gamma, beta, nullptr,
+                         save_var, dgamma, dbeta, eps, slope, N, C, HW, workspace,
+                         workspace_bytes, stream);
 }
 
 }  // extern "C"

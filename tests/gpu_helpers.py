@@ -33,27 +33,28 @@ def to_f64(t: torch.Tensor) -> np.ndarray:
     return t.detach().to("cpu").to(torch.float64).numpy()
 
 
-def max_rel(got: np.ndarray, ref: np.ndarray, floor_frac: float = 1e-3) -> float:
-    """max_i |got_i - ref_i| / max(|ref_i|, floor_frac * max_j |ref_j|)."""
+def max_rel(got: np.ndarray, ref: np.ndarray, floor_frac: float = 1e-3,
+            floor_abs: float = 0.0) -> float:
+    """max_i |got_i - ref_i| / max(|ref_i|, floor_frac * max_j |ref_j|, floor_abs)."""
     got = np.asarray(got, dtype=np.float64)
     ref = np.asarray(ref, dtype=np.float64)
     if ref.size == 0:
         return 0.0
     scale = np.max(np.abs(ref))
-    denom = np.maximum(np.abs(ref), floor_frac * scale)
+    denom = np.maximum(np.maximum(np.abs(ref), floor_frac * scale), floor_abs)
     denom = np.where(denom > 0, denom, 1.0)
     return float(np.max(np.abs(got - ref) / denom))
 
 
-def assert_close(name: str, got, ref, dtype: str, mask=None) -> float:
+def assert_close(name: str, got, ref, dtype: str, mask=None, floor_abs: float = 0.0) -> float:
     got = np.asarray(got, dtype=np.float64)
     ref = np.asarray(ref, dtype=np.float64)
     assert got.shape == ref.shape, (name, got.shape, ref.shape)
     assert np.all(np.isfinite(got)), "%s has non-finite values" % name
     if mask is not None:
-        err = max_rel(got[mask], ref[mask]) if mask.any() else 0.0
+        err = max_rel(got[mask], ref[mask], floor_abs=floor_abs) if mask.any() else 0.0
     else:
-        err = max_rel(got, ref)
+        err = max_rel(got, ref, floor_abs=floor_abs)
     tol = TOL[dtype]
     assert err <= tol, "%s: max rel err %.3e > %.1e (%s)" % (name, err, tol, dtype)
     return err

@@ -185,6 +185,64 @@ def test_phase_entry_points_validate(lib):
                                    4, FAKE, 1 << 20, STREAM) == ERR_NULL
 
 
+@no_gpu
+def test_comparison_blocks_validate(lib):
+    """The other blocks' entry points reject the same bad arguments, plus their
+    extra tensors (z for the standard and checkpointing forwards, z and the
+    saved mean for the standard backward) when NULL."""
+    def sfwd(x=FAKE, z=FAKE, ptrs=None, mom=0.1, slope=0.01, N=2, C=3, HW=4, wsb=1 << 20):
+        ptrs = ptrs or [FAKE] * 6
+        return lib.iabn_std_forward_train(x, z, F16, *ptrs, 1e-5, mom, slope, N, C, HW, FAKE, wsb,
+                                          STREAM)
+
+    def cfwd(x=FAKE, z=FAKE, ptrs=None, mom=0.1, slope=0.01, N=2, C=3, HW=4, wsb=1 << 20):
+        ptrs = ptrs or [FAKE] * 6
+        return lib.iabn_ckpt_forward_train(x, z, BF16, *ptrs, 1e-5, mom, slope, N, C, HW, FAKE,
+                                           wsb, STREAM)
+
+    for f in (sfwd, cfwd):
+        assert f(x=NULL) == ERR_NULL
+        assert f(z=NULL) == ERR_NULL
+        for k in range(6):
+            ptrs = [FAKE] * 6
+            ptrs[k] = NULL
+            assert f(ptrs=ptrs) == ERR_NULL
+        assert f(mom=2.0) == ERR_PARAM
+        assert f(slope=-1.0) == ERR_PARAM
+        assert f(N=1, HW=1) == ERR_SHAPE
+        assert f(wsb=4) == ERR_WORKSPACE
+        assert f(x=NULL, z=NULL, ptrs=[NULL] * 6, C=0) == OK
+
+    def sbw(x=FAKE, z=FAKE, dz=FAKE, ptrs=None, eps=1e-5, wsb=1 << 20):
+        ptrs = ptrs or [FAKE] * 6
+        return lib.iabn_std_backward(x, z, dz, F32, *ptrs, eps, 0.01, 2, 3, 4, FAKE, wsb, STREAM)
+    for kw in ("x", "z", "dz"):
+        assert sbw(**{kw: NULL}) == ERR_NULL
+    for k in range(6):
+        ptrs = [FAKE] * 6
+        ptrs[k] = NULL
+        assert sbw(ptrs=ptrs) == ERR_NULL
+    assert sbw(eps=0.0) == ERR_PARAM
+    assert sbw(wsb=0) == ERR_WORKSPACE
+
+    for fn in (lib.iabn_backward_ii, lib.iabn_ckpt_backward):
+        assert fn(NULL, FAKE, F16, *([FAKE] * 5), 1e-5, 0.01, 2, 3, 4, FAKE, 1 << 20,
+                  STREAM) == ERR_NULL
+        assert fn(FAKE, FAKE, F16, *([FAKE] * 4), NULL, 1e-5, 0.01, 2, 3, 4, FAKE, 1 << 20,
+                  STREAM) == ERR_NULL
+        assert fn(FAKE, FAKE, F16, *([FAKE] * 5), 1e-5, 0.0, 2, 3, 4, FAKE, 1 << 20,
+                  STREAM) == ERR_PARAM
+        assert fn(FAKE, FAKE, 9, *([FAKE] * 5), 1e-5, 0.01, 2, 3, 4, FAKE, 1 << 20,
+                  STREAM) == ERR_DTYPE
+
+    assert lib.iabn_ckpt_recompute(NULL, FAKE, F32, FAKE, FAKE, 0.01, 2, 3, 4, STREAM) == ERR_NULL
+    assert lib.iabn_ckpt_recompute(FAKE, FAKE, F32, FAKE, NULL, 0.01, 2, 3, 4, STREAM) == ERR_NULL
+    assert lib.iabn_ckpt_recompute(FAKE, FAKE, F32, FAKE, FAKE, 0.0, 2, 3, 4, STREAM) == ERR_PARAM
+    assert lib.iabn_ckpt_recompute(FAKE, FAKE, F32, FAKE, FAKE, 0.01, -2, 3, 4, STREAM) == ERR_SHAPE
+    # one value per channel is fine without statistics
+    assert lib.iabn_ckpt_recompute(NULL, NULL, F32, NULL, NULL, 0.01, 2, 0, 4, STREAM) == OK
+
+
 def test_binding_rejects_bad_tensors():
     # Marshalling checks in the binding run before any library call.
     x = torch.zeros(2, 3, 4)
