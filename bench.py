@@ -61,6 +61,9 @@ def parse():
     ap.add_argument("--config", type=int, default=5, help="workload index (1-5)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="time budget of the oracle baseline (0 disables it)")
+    ap.add_argument("--no-arms", action="store_true",
+                    help="skip timing the other blocks of Sec. 3.2 (InPlace-ABN II, standard, "
+                         "checkpointing) on the same workload")
     ap.add_argument("--phase-kernels", action="store_true",
                     help="also time the phase entry points (the streaming kernels), one by one")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -134,6 +137,88 @@ def time_phases(lib, layers, refresh, check, stream, steps, b):
 
 class Layer:
     pass
+
+
+def time_arms(lib, layers, refresh, check, stream, args, E_total, b, iabn_kernels, dev, sp, code,
+              w, wsp, ws_bytes):
+    """The same step for the other blocks of Sec. 3.2, each through its own
+    entry points over the same layers: InPlace-ABN II (backward from z in
+    terms of y), the standard block (keeps x and z; backward from x with the
+    signs of z) and the proposed checkpointing (keeps xhat; the backward
+    recomputes z from xhat, then runs from xhat).  Per block: ms per step,
+    average forward / backward time per layer, algorithmic bytes per element
+    (units of the storage size b) and the activation bytes kept for the
+    backward."""
+    import torch
+    p = lambda t: ctypes.c_void_p(t.data_ptr())  # noqa: E731
+    zmax = max(L.E for L in layers)
+    ztmp = torch.empty(zmax, dtype=layers[0].x.dtype, device=dev)  # checkpointing's transient z
+    for L in layers:
+        N, C, HW = L.shape
+        L.zs = torch.empty_like(L.x)  # the standard block's stored z
+        common = (w.eps, w.momentum, w.slope, N, C, HW, wsp, ws_bytes, sp)
+        L.std_fwd = (p(L.x), p(L.zs), code, p(L.gamma), p(L.beta), p(L.rm), p(L.rv), p(L.sm),
+                     p(L.sv)) + common
+        L.std_bwd = (p(L.x), p(L.zs), p(L.dz), code, p(L.gamma), p(L.beta), p(L.sm), p(L.sv),
+                     p(L.dg), p(L.db), w.eps, w.slope, N, C, HW, wsp, ws_bytes, sp)
+        L.ck_fwd = (p(L.x), p(ztmp), code, p(L.gamma), p(L.beta), p(L.rm), p(L.rv), p(L.sm),
+                    p(L.sv)) + common
+        L.ck_rec = (p(L.x), p(ztmp), code, p(L.gamma), p(L.beta), w.slope, N, C, HW, sp)
+        L.ck_bwd = (p(L.x), p(L.dz), code, p(L.gamma), p(L.beta), p(L.sv), p(L.dg), p(L.db),
+                    w.eps, w.slope, N, C, HW, wsp, ws_bytes, sp)
+    blocks = {
+        "inplace_abn_ii": ([(lib.iabn_forward_train, "fwd")],
+                           [(lib.iabn_backward_ii, "bwd")], 2, 3, 1),
+        "standard": ([(lib.iabn_std_forward_train, "std_fwd")],
+                     [(lib.iabn_std_backward, "std_bwd")], 2, 4, 2),
+        "checkpointing": ([(lib.iabn_ckpt_forward_train, "ck_fwd")],
+                          [(lib.iabn_ckpt_recompute, "ck_rec"), (lib.iabn_ckpt_backward, "ck_bwd")],
+                          3, 5, 1),
+    }
+    out = {}
+    for name, (fcalls, bcalls, fb, bb, kept) in blocks.items():
+        def fwd_pass():
+            for L in layers:
+                for fn, attr in fcalls:
+                    check(fn(*getattr(L, attr)), name)
+
+        def bwd_pass():
+            for L in reversed(layers):
+                for fn, attr in bcalls:
+                    check(fn(*getattr(L, attr)), name)
+        refresh()
+        for _ in range(args.warmup):
+            fwd_pass()
+            bwd_pass()
+        torch.cuda.synchronize()
+        refresh()
+        torch.cuda.synchronize()
+        marks = [torch.cuda.Event(enable_timing=True) for _ in range(2 * args.steps + 1)]
+        t0 = time.perf_counter()
+        for i in range(args.steps):
+            marks[2 * i].record(stream)
+            fwd_pass()
+            marks[2 * i + 1].record(stream)
+            bwd_pass()
+        marks[-1].record(stream)
+        torch.cuda.synchronize()
+        ms = (time.perf_counter() - t0) * 1e3 / args.steps
+        fwd_ms = sum(marks[2 * i].elapsed_time(marks[2 * i + 1]) for i in range(args.steps))
+        bwd_ms = sum(marks[2 * i + 1].elapsed_time(marks[2 * i + 2]) for i in range(args.steps))
+        n = args.steps * len(layers)
+        out[name] = {"ms_per_step": round(ms, 4), "value": round(E_total / (ms * 1e-3), 1),
+                     "forward_avg_us": round(fwd_ms / n * 1e3, 3),
+                     "backward_avg_us": round(bwd_ms / n * 1e3, 3),
+                     "alg_bytes_per_elem_b": {"forward": fb, "backward": bb},
+                     "alg_gbps": round((fb + bb) * E_total * b * args.steps / ((fwd_ms + bwd_ms) * 1e-3) / 1e9, 1),
+                     "stored_activation_bytes": kept * E_total * b}
+    iabn_us = (iabn_kernels["iabn_forward_train"]["avg_us"] + iabn_kernels["iabn_backward"]["avg_us"])
+    std_us = out["standard"]["forward_avg_us"] + out["standard"]["backward_avg_us"]
+    out["inplace_abn_time_vs_standard"] = round(iabn_us / std_us - 1.0, 4)
+    out["inplace_abn_memory_vs_standard"] = 0.5
+    for L in layers:
+        del L.zs
+    return out
 
 
 def main():
@@ -293,6 +378,13 @@ def measure(lib, args):
                 "traffic": measured_traffic(dom, args.config)}
     log("entry points: " + json.dumps(kernels))
 
+    # ---------------------------------------------------------------- other blocks
+    arms = None
+    if not args.no_arms:
+        arms = time_arms(lib, layers, refresh, check, stream, args, E_total, b, kernels, dev, sp,
+                         code, w, wsp, ws_bytes)
+        log("blocks: " + json.dumps(arms))
+
     # ---------------------------------------------------------------- phase kernels
     phase_kernels = None
     if args.phase_kernels:
@@ -366,6 +458,7 @@ def measure(lib, args):
         "activation_memory": {"iabn_stored_bytes": E_total * b,
                               "store_x_baseline_bytes": 2 * E_total * b},
         "kernels": kernels,
+        "blocks": arms,
         "phase_kernels": phase_kernels,
         "roofline": roofline,
         "cpu_baseline": cpu,
