@@ -184,3 +184,48 @@ def workload_layer(w: Workload, layer: int, threads: int = 0) -> LayerInputs:
     N, C, HW = w.layers[layer]
     return make_layer(N, C, HW, w.dtype, w.seed, layer, dz_std=w.dz_std,
                       gamma_sign=w.gamma_sign, threads=threads)
+
+
+def make_layer_device(N: int, C: int, HW: int, dtype: str, seed: int, dz_std: float = 0.1,
+                      gamma_sign: bool = False, device="cuda"):
+    """One layer drawn directly on the device, for tensors too large to build
+    on the host: the per-channel parameters follow the module recipe (numpy,
+    ``SeedSequence([seed, 0])``); x and dz are drawn channel by channel with
+    torch's seeded device generator (Philox) in float32 and rounded to the
+    storage type (round to nearest even).  Same distributions as
+    ``make_layer``, a different stream of numbers.
+
+    Returns ``(x, dz, params)``: device tensors of shape (N, C, HW) in the
+    storage type and a ``LayerInputs`` whose x/dz are None.
+    """
+    import torch
+
+    if dtype not in DTYPES:
+        raise ValueError("unknown dtype %r" % dtype)
+    prng = _rng(seed, 0)
+    mu = prng.uniform(-2.0, 2.0, C)
+    sigma = prng.uniform(0.5, 3.0, C)
+    gamma = prng.uniform(0.5, 1.5, C)
+    if gamma_sign:
+        gamma = gamma * np.where(prng.uniform(0.0, 1.0, C) < 0.5, -1.0, 1.0)
+    beta = prng.normal(0.0, 0.1, C)
+    tdt = {"f32": torch.float32, "f16": torch.float16, "bf16": torch.bfloat16}[dtype]
+    x = torch.empty((N, C, HW), dtype=tdt, device=device)
+    dz = torch.empty((N, C, HW), dtype=tdt, device=device)
+    g = torch.Generator(device=device)
+    g.manual_seed(int(seed))
+    # Channel by channel while channels are large, in groups otherwise.
+    step = max(1, (1 << 26) // max(1, N * HW))
+    for c0 in range(0, C, step):
+        c1 = min(C, c0 + step)
+        mu_t = torch.tensor(mu[c0:c1], dtype=torch.float32, device=device)[None, :, None]
+        sd_t = torch.tensor(sigma[c0:c1], dtype=torch.float32, device=device)[None, :, None]
+        r = torch.randn((N, c1 - c0, HW), generator=g, device=device, dtype=torch.float32)
+        x[:, c0:c1] = (r * sd_t + mu_t).to(tdt)
+        r = torch.randn((N, c1 - c0, HW), generator=g, device=device, dtype=torch.float32)
+        dz[:, c0:c1] = (r * float(dz_std)).to(tdt)
+        del r
+    params = LayerInputs(x=None, dz=None, gamma=gamma.astype(np.float32),
+                         beta=beta.astype(np.float32), running_mean=np.zeros(C, np.float32),
+                         running_var=np.ones(C, np.float32), dtype=dtype)
+    return x, dz, params
