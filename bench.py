@@ -406,28 +406,37 @@ def measure(lib, args):
             for v in groups.values():
                 if r < len(v):
                     order.append(v[r])
+        # Passes over the layers repeat until the budget is spent (the whole
+        # sweep can take less than the budget).
         spent = 0.0
         done = 0
         used = []
-        for li in order:
-            inp = host_layers[li]
-            x = workloads.storage_to_f64(inp.x, w.dtype)
-            dz = workloads.storage_to_f64(inp.dz, w.dtype)
-            c0 = time.perf_counter()
-            fw = oracle.forward_train(x, inp.gamma, inp.beta, inp.running_mean, inp.running_var,
-                                      w.eps, w.momentum, w.slope)
-            oracle.backward_i(fw["z"], dz, inp.gamma, inp.beta, fw["var"], w.eps, w.slope)
-            spent += time.perf_counter() - c0
-            done += x.size
-            used.append(li)
-            del x, dz, fw
-            if spent >= args.cpu_seconds:
-                break
+        f64 = {}
+        while spent < args.cpu_seconds:
+            for li in order:
+                inp = host_layers[li]
+                if li not in f64:
+                    f64[li] = (workloads.storage_to_f64(inp.x, w.dtype),
+                               workloads.storage_to_f64(inp.dz, w.dtype))
+                x, dz = f64[li]
+                c0 = time.perf_counter()
+                fw = oracle.forward_train(x, inp.gamma, inp.beta, inp.running_mean,
+                                          inp.running_var, w.eps, w.momentum, w.slope)
+                oracle.backward_i(fw["z"], dz, inp.gamma, inp.beta, fw["var"], w.eps, w.slope)
+                spent += time.perf_counter() - c0
+                done += x.size
+                used.append(li)
+                del fw
+                if spent >= args.cpu_seconds:
+                    break
+        del f64
+        passes = len(used) / len(order)
         cpu = {"value": round(done / spent, 1), "unit": "elements/s", "cores": oracle.num_threads(),
                "kind": "oracle",
-               "sample": "oracle fp64 forward_train + backward_i over whole layers %s of %s "
-                         "(%.3g elements, %.1f s), inputs already in fp64" % (used, w.name, done,
-                                                                           spent)}
+               "sample": "oracle fp64 forward_train + backward_i over %.2f passes of the %d layers "
+                         "of %s, shape groups interleaved (%.3g elements, %.1f s of oracle time); "
+                         "inputs converted to fp64 outside the timing" % (passes, len(order),
+                                                                          w.name, done, spent)}
         log("cpu baseline: %.3g elements/s on %d threads" % (cpu["value"], cpu["cores"]))
 
     out = {
@@ -447,12 +456,14 @@ def measure(lib, args):
                    "elements_per_tensor": E_total, "slope": w.slope, "eps": w.eps,
                    "momentum": w.momentum},
         # floor: every tensor crosses HBM once (x in, z out, z and dz in, dx
-        # out); schedule: the two-pass streaming schedule (x, z, dz read twice).
-        "hbm": {"schedule_bytes_per_step": sched_bytes,
-                "schedule_gbps": round(sched_bytes / (ms_per_step * 1e-3) / 1e9, 1),
-                "schedule_frac_of_peak": round(sched_bytes / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
-                "floor_bytes_per_step": floor_bytes,
-                "floor_gbps": round(floor_bytes / (ms_per_step * 1e-3) / 1e9, 1)},
+        # out), which is what the channel-resident kernels move; the two-pass
+        # streaming schedule (x, z and dz read twice) is not what runs, its
+        # bytes over the step time are only an equivalent rate.
+        "hbm": {"floor_bytes_per_step": floor_bytes,
+                "floor_gbps": round(floor_bytes / (ms_per_step * 1e-3) / 1e9, 1),
+                "floor_frac_of_peak": round(floor_bytes / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
+                "two_pass_schedule_bytes_per_step": sched_bytes,
+                "two_pass_schedule_equivalent_gbps": round(sched_bytes / (ms_per_step * 1e-3) / 1e9, 1)},
         "event_ms_per_step": round(ev_ms_per_step, 4),
         "outputs_finite": finite,
         "activation_memory": {"iabn_stored_bytes": E_total * b,
