@@ -73,12 +73,15 @@ def parse():
 
 
 def kernel_source_digest() -> str:
-    """sha256 of the sources libiabn.so is built from."""
+    """sha256 of the sources libiabn.so is built from (csrc/ and the header)."""
+    import glob
     import hashlib
     h = hashlib.sha256()
-    for rel in ("paper_1712_02616_amd/csrc/iabn.hip", "paper_1712_02616_amd/csrc/divmagic.h",
-                "include/iabn.h"):
-        with open(os.path.join(ROOT, rel), "rb") as f:
+    csrc = os.path.join(ROOT, "paper_1712_02616_amd", "csrc")
+    files = sorted(glob.glob(os.path.join(csrc, "*.hip")) + glob.glob(os.path.join(csrc, "*.h")))
+    for path in files + [os.path.join(ROOT, "include", "iabn.h")]:
+        h.update(os.path.relpath(path, ROOT).encode())
+        with open(path, "rb") as f:
             h.update(f.read())
     return h.hexdigest()
 

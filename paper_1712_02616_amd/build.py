@@ -1,17 +1,29 @@
-"""Compile libiabn.so (the HIP kernels and the C ABI) for gfx950 with hipcc."""
+"""Compile libiabn.so (the HIP kernels and the C ABI) for gfx950 with hipcc.
+
+Each translation unit of ``csrc/`` compiles to an object file in parallel,
+then one link makes the shared library.
+"""
 
 from __future__ import annotations
 
+import glob
 import os
 import shutil
 import subprocess
+import tempfile
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
-SOURCES = [os.path.join(HERE, "csrc", "iabn.hip")]
-HEADERS = [os.path.join(HERE, "csrc", "divmagic.h"), os.path.join(ROOT, "include", "iabn.h")]
+CSRC = os.path.join(HERE, "csrc")
+SOURCES = sorted(glob.glob(os.path.join(CSRC, "*.hip")))
+HEADERS = sorted(glob.glob(os.path.join(CSRC, "*.h"))) + [os.path.join(ROOT, "include", "iabn.h")]
 LIB = os.path.join(HERE, "libiabn.so")
 ARCH = "gfx950"
+
+FLAGS = ["--offload-arch=" + ARCH, "-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-function",
+         # Packed fp32 VALU instructions stay off on this target.
+         "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+         "-I", os.path.join(ROOT, "include"), "-I", CSRC]
 
 
 def hipcc() -> str:
@@ -21,25 +33,35 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found; it is needed to build libiabn.so")
 
 
-def command(out: str) -> list:
-    return [hipcc(), "--offload-arch=" + ARCH, "-O3", "-std=c++17", "-fPIC", "-shared",
-            "-Wall", "-Wno-unused-function",
-            # Packed fp32 VALU instructions stay off on this target.
-            "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-            "-I", os.path.join(ROOT, "include"), "-I", os.path.join(HERE, "csrc"),
-            "-o", out] + SOURCES
+def _run(cmd):
+    return subprocess.Popen(cmd, stdout=subprocess.PIPE, stderr=subprocess.PIPE, text=True)
 
 
 def build(verbose: bool = False) -> str:
     """Always recompiles; writes libiabn.so next to this file atomically."""
-    tmp = LIB + ".tmp%d" % os.getpid()
-    cmd = command(tmp)
-    res = subprocess.run(cmd, capture_output=True, text=True)
-    if res.returncode != 0:
-        raise RuntimeError("hipcc failed (%d):\n%s\n%s" % (res.returncode, " ".join(cmd), res.stderr))
-    if verbose and res.stderr:
-        print(res.stderr)
-    os.replace(tmp, LIB)
+    cc = hipcc()
+    with tempfile.TemporaryDirectory(prefix="iabn_build_") as tmp:
+        objs, procs = [], []
+        for src in SOURCES:
+            obj = os.path.join(tmp, os.path.basename(src) + ".o")
+            cmd = [cc] + FLAGS + ["-c", "-o", obj, src]
+            objs.append(obj)
+            procs.append((cmd, _run(cmd)))
+        errors = []
+        for cmd, p in procs:
+            out, err = p.communicate()
+            if p.returncode != 0:
+                errors.append("%s\n%s" % (" ".join(cmd), err))
+            elif verbose and err:
+                print(err)
+        if errors:
+            raise RuntimeError("hipcc failed:\n" + "\n".join(errors))
+        out = LIB + ".tmp%d" % os.getpid()
+        cmd = [cc, "--offload-arch=" + ARCH, "-shared", "-fPIC", "-o", out] + objs
+        res = subprocess.run(cmd, capture_output=True, text=True)
+        if res.returncode != 0:
+            raise RuntimeError("link failed (%d):\n%s\n%s" % (res.returncode, " ".join(cmd), res.stderr))
+        os.replace(out, LIB)
     return LIB
 
 

@@ -1,0 +1,437 @@
+// The C ABI of libiabn (include/iabn.h): argument validation on the host
+// before any launch, the choice between the channel-resident and the
+// streaming kernels, and the entry points themselves.
+
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <cmath>
+
+#include "launch.h"
+
+#define IABN_VERSION 10100
+
+namespace iabn_impl {
+namespace {
+
+thread_local char g_last_error[256] = "";
+
+int fail(int code, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+int fail(int code, const char* fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_last_error, sizeof g_last_error, fmt, ap);
+    va_end(ap);
+    return code;
+}
+
+int ok() {
+    g_last_error[0] = '\0';
+    return IABN_OK;
+}
+
+constexpr int64_t kMaxChannelElems = (int64_t(1) << 31) - 1;
+constexpr int64_t kMaxChannels = int64_t(1) << 20;
+constexpr int64_t kMaxTotalElems = int64_t(1) << 46;
+constexpr int64_t kTargetBlocks = 512;     // 2 blocks of 4 waves per CU on 256 CUs (measured best)
+constexpr int64_t kMinSliceElems = 4096;   // at least 16 elements per thread
+constexpr int64_t kMaxSlices = 1024;
+constexpr int64_t kSliceAlign = 8;         // slices start on a 16-byte access of any dtype
+
+int elem_bytes(int dtype) { return dtype == IABN_F32 ? 4 : 2; }
+
+bool valid_dtype(int dtype) { return dtype == IABN_F32 || dtype == IABN_F16 || dtype == IABN_BF16; }
+
+// Slices per channel and slice length in elements; depends on the shape only.
+struct Split {
+    int64_t P;
+    int64_t L;
+};
+
+Split split_channel(int64_t m, int64_t C) {
+    int64_t P = (kTargetBlocks + C - 1) / C;
+    const int64_t pmax_len = (m + kMinSliceElems - 1) / kMinSliceElems;
+    if (P > pmax_len) P = pmax_len;
+    if (P > kMaxSlices) P = kMaxSlices;
+    if (P < 1) P = 1;
+    int64_t L = (m + P - 1) / P;
+    L = (L + kSliceAlign - 1) / kSliceAlign * kSliceAlign;
+    P = (m + L - 1) / L;
+    return {P, L};
+}
+
+// Validates the shape; `train` also needs N*HW >= 2.
+int check_shape(int64_t N, int64_t C, int64_t HW, bool train) {
+    if (N < 0 || C < 0 || HW < 0)
+        return fail(IABN_ERR_SHAPE, "negative size N=%lld C=%lld HW=%lld", (long long)N,
+                    (long long)C, (long long)HW);
+    if (C > kMaxChannels) return fail(IABN_ERR_SHAPE, "C=%lld exceeds 2^20", (long long)C);
+    if (N != 0 && HW > kMaxChannelElems / N)
+        return fail(IABN_ERR_SHAPE, "N*HW exceeds 2^31-1");
+    if (C != 0 && N * HW > kMaxTotalElems / C)
+        return fail(IABN_ERR_SHAPE, "N*C*HW exceeds 2^46");
+    if (train && C > 0 && N * HW < 2)
+        return fail(IABN_ERR_SHAPE, "training needs N*HW >= 2 values per channel, got %lld",
+                    (long long)(N * HW));
+    return IABN_OK;
+}
+
+size_t workspace_bytes_for(int64_t N, int64_t C, int64_t HW) {
+    if (C == 0 || N * HW == 0) return 0;
+    const Split sp = split_channel(N * HW, C);
+    return static_cast<size_t>(C) * static_cast<size_t>(sp.P) * kWaves * sizeof(Partial);
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// The access geometry.  vector=true uses 16-byte accesses (requires
+// HW % (16/elem) == 0 and 16-byte aligned pointers).
+Geom make_geom(int64_t N, int64_t C, int64_t HW, int dtype, bool vector) {
+    const int64_t m = N * HW;
+    const Split sp = split_channel(m, C);
+    const int64_t vec = vector ? 16 / elem_bytes(dtype) : 1;
+    Geom g;
+    g.C = static_cast<uint32_t>(C);
+    g.P = static_cast<uint32_t>(sp.P);
+    g.vrow = static_cast<uint32_t>(HW / vec);
+    g.vchan = static_cast<uint32_t>(m / vec);
+    g.lv = static_cast<uint32_t>(sp.L / vec);
+    g.vec = static_cast<uint32_t>(vec);
+    g.row_div = iabn_divmagic_make(g.vrow);
+    g.nstride = static_cast<uint64_t>(C) * g.vrow;
+    g.m = static_cast<double>(m);
+    return g;
+}
+
+bool use_vector(int64_t HW, int dtype, const void* a, const void* b) {
+    const int64_t vec = 16 / elem_bytes(dtype);
+    return HW % vec == 0 && aligned16(a) && (b == nullptr || aligned16(b));
+}
+
+int check_workspace(int64_t N, int64_t C, int64_t HW, const void* ws, size_t bytes) {
+    const size_t need = workspace_bytes_for(N, C, HW);
+    if (need == 0) return IABN_OK;
+    if (ws == nullptr) return fail(IABN_ERR_NULL, "workspace is NULL (%zu bytes needed)", need);
+    if (bytes < need)
+        return fail(IABN_ERR_WORKSPACE, "workspace has %zu bytes, %zu needed", bytes, need);
+    if ((reinterpret_cast<uintptr_t>(ws) & 15u) != 0)
+        return fail(IABN_ERR_WORKSPACE, "workspace is not 16-byte aligned");
+    return IABN_OK;
+}
+
+int check_params(float eps, float slope) {
+    if (!(eps > 0.f) || !std::isfinite(eps)) return fail(IABN_ERR_PARAM, "eps must be finite and > 0");
+    if (!(slope > 0.f) || !std::isfinite(slope))
+        return fail(IABN_ERR_PARAM, "slope must be finite and > 0 (the activation must be invertible)");
+    return IABN_OK;
+}
+
+int launched(const char* what) {
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return fail(IABN_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+    return ok();
+}
+
+int validate_common(int dtype, int64_t N, int64_t C, int64_t HW, bool train) {
+    if (!valid_dtype(dtype)) return fail(IABN_ERR_DTYPE, "unknown dtype %d", dtype);
+    return check_shape(N, C, HW, train);
+}
+
+bool empty(int64_t N, int64_t C, int64_t HW) { return C == 0 || N * HW == 0; }
+
+bool vector_ok(int64_t HW, int dtype, const void* a, const void* b, const void* c) {
+    return use_vector(HW, dtype, a, b) && (c == nullptr || aligned16(c));
+}
+
+const char* fwd_name(int fm) {
+    return fm == kFwdOut ? "standard forward" : fm == kFwdCkpt ? "checkpointing forward" : "forward";
+}
+
+// Training forward of the three arms (fm: kFwdInPlace, kFwdOut, kFwdCkpt).
+// x is the input (kFwdInPlace: z on return; kFwdCkpt: xhat on return); out
+// receives z for kFwdOut and kFwdCkpt.  Everything is validated before the
+// first launch, so an error changes nothing.
+int forward_train_impl(int fm, void* x, void* out, int dtype, const float* gamma,
+                       const float* beta, float* running_mean, float* running_var,
+                       float* save_mean, float* save_var, float eps, float momentum, float slope,
+                       int64_t N, int64_t C, int64_t HW, void* workspace, size_t workspace_bytes,
+                       void* stream) {
+    int rc = validate_common(dtype, N, C, HW, true);
+    if (rc) return rc;
+    if (empty(N, C, HW)) return ok();
+    if (!x || !gamma || !beta || !running_mean || !running_var || !save_mean || !save_var ||
+        (fm != kFwdInPlace && !out))
+        return fail(IABN_ERR_NULL, "a tensor or parameter pointer is NULL");
+    if ((rc = check_params(eps, slope))) return rc;
+    if (!(momentum >= 0.f && momentum <= 1.f))
+        return fail(IABN_ERR_PARAM, "momentum must lie in [0, 1]");
+    if ((rc = check_workspace(N, C, HW, workspace, workspace_bytes))) return rc;
+    const bool vec = use_vector(HW, dtype, x, fm == kFwdInPlace ? nullptr : out);
+    const Geom g = make_geom(N, C, HW, dtype, vec);
+    const FwdParams prm = {gamma,    beta, running_mean, running_var, save_mean, save_var,
+                           fm == kFwdInPlace ? nullptr : out, eps, momentum, slope};
+    const hipStream_t st = static_cast<hipStream_t>(stream);
+    FusedPlan fp;
+    if (plan_fused(C, g, vec, false, &fp)) {
+        if (!launch_fwd_fused(dtype, fm, x, g, fp, prm, st))
+            return fail(IABN_ERR_HIP, "no %s kernel built for T=%d R=%d", fwd_name(fm), fp.T, fp.R);
+        return launched(fwd_name(fm));
+    }
+    Partial* part = static_cast<Partial*>(workspace);
+    launch_fwd_stats(dtype, vec, static_cast<const void*>(x), g, part, st);
+    if ((rc = launched("fwd_stats"))) return rc;
+    launch_fwd_apply(dtype, vec, x, g, static_cast<const Partial*>(part), prm, true, fm, st);
+    return launched(fwd_name(fm));
+}
+
+const char* bwd_name(int bm, bool ii) {
+    return bm == kBwdFromXZ     ? "standard backward"
+           : bm == kBwdFromXhat ? "checkpointing backward"
+           : ii                 ? "backward (formulation II)"
+                                : "backward";
+}
+
+// Backward of every formulation (bm, ii: see BwdSign).  u is z, x or xhat;
+// zs is the stored z for kBwdFromXZ; dz_dx holds dz on entry, dx on return.
+int backward_impl(int bm, bool ii, const void* u, const void* zs, void* dz_dx, int dtype,
+                  const float* gamma, const float* beta, const float* save_mean,
+                  const float* save_var, float* dgamma, float* dbeta, float eps, float slope,
+                  int64_t N, int64_t C, int64_t HW, void* workspace, size_t workspace_bytes,
+                  void* stream) {
+    int rc = validate_common(dtype, N, C, HW, true);
+    if (rc) return rc;
+    if (empty(N, C, HW)) return ok();
+    if (!u || !dz_dx || !gamma || !beta || !save_var || !dgamma || !dbeta ||
+        (bm == kBwdFromXZ && (!zs || !save_mean)))
+        return fail(IABN_ERR_NULL, "a tensor or parameter pointer is NULL");
+    if ((rc = check_params(eps, slope))) return rc;
+    if ((rc = check_workspace(N, C, HW, workspace, workspace_bytes))) return rc;
+    const bool vec = vector_ok(HW, dtype, u, dz_dx, bm == kBwdFromXZ ? zs : nullptr);
+    const Geom g = make_geom(N, C, HW, dtype, vec);
+    const BwdParams prm = {gamma, beta, save_mean, save_var, dgamma, dbeta, eps, slope, ii ? 1 : 0};
+    const hipStream_t st = static_cast<hipStream_t>(stream);
+    FusedPlan fp;
+    if (plan_fused(C, g, vec, true, &fp)) {
+        if (!launch_bwd_fused(dtype, bm, u, zs, dz_dx, g, fp, prm, st))
+            return fail(IABN_ERR_HIP, "no %s kernel built for T=%d R=%d", bwd_name(bm, ii), fp.T, fp.R);
+        return launched(bwd_name(bm, ii));
+    }
+    Partial* part = static_cast<Partial*>(workspace);
+    launch_bwd_reduce(dtype, vec, u, zs, static_cast<const void*>(dz_dx), g, prm, bm, part, st);
+    if ((rc = launched("bwd_reduce"))) return rc;
+    launch_bwd_apply(dtype, vec, u, zs, dz_dx, g, static_cast<const Partial*>(part), prm, bm, st);
+    return launched(bwd_name(bm, ii));
+}
+
+}  // namespace
+}  // namespace iabn_impl
+
+using namespace iabn_impl;
+
+
+// ---------------------------------------------------------------- C ABI
+
+extern "C" {
+
+int iabn_version(void) { return IABN_VERSION; }
+
+const char* iabn_status_string(int status) {
+    switch (status) {
+        case IABN_OK: return "IABN_OK";
+        case IABN_ERR_NULL: return "IABN_ERR_NULL: a required pointer is NULL";
+        case IABN_ERR_SHAPE: return "IABN_ERR_SHAPE: invalid tensor shape";
+        case IABN_ERR_PARAM: return "IABN_ERR_PARAM: eps, momentum or slope out of range";
+        case IABN_ERR_DTYPE: return "IABN_ERR_DTYPE: unknown storage type";
+        case IABN_ERR_WORKSPACE: return "IABN_ERR_WORKSPACE: workspace too small or misaligned";
+        case IABN_ERR_HIP: return "IABN_ERR_HIP: the HIP runtime rejected a launch";
+        default: return "unknown iabn status";
+    }
+}
+
+const char* iabn_last_error(void) { return g_last_error; }
+
+size_t iabn_workspace_size(int64_t N, int64_t C, int64_t HW, int dtype) {
+    if (!valid_dtype(dtype)) return 0;
+    if (check_shape(N, C, HW, false) != IABN_OK) return 0;
+    return workspace_bytes_for(N, C, HW);
+}
+
+int iabn_forward_stats(const void* x, int dtype, int64_t N, int64_t C, int64_t HW,
+                       void* workspace, size_t workspace_bytes, void* stream) {
+    int rc = validate_common(dtype, N, C, HW, true);
+    if (rc) return rc;
+    if (empty(N, C, HW)) return ok();
+    if (x == nullptr) return fail(IABN_ERR_NULL, "x is NULL");
+    if ((rc = check_workspace(N, C, HW, workspace, workspace_bytes))) return rc;
+    const bool vec = use_vector(HW, dtype, x, nullptr);
+    const Geom g = make_geom(N, C, HW, dtype, vec);
+    launch_fwd_stats(dtype, vec, x, g, static_cast<Partial*>(workspace),
+                             static_cast<hipStream_t>(stream));
+    return launched("fwd_stats");
+}
+
+int iabn_forward_apply(void* x_z, int dtype, const float* gamma, const float* beta,
+                       float* running_mean, float* running_var, float* save_mean,
+                       float* save_var, float eps, float momentum, float slope, int64_t N,
+                       int64_t C, int64_t HW, void* workspace, size_t workspace_bytes,
+                       void* stream) {
+    int rc = validate_common(dtype, N, C, HW, true);
+    if (rc) return rc;
+    if (empty(N, C, HW)) return ok();
+    if (!x_z || !gamma || !beta || !running_mean || !running_var || !save_mean || !save_var)
+        return fail(IABN_ERR_NULL, "a tensor or parameter pointer is NULL");
+    if ((rc = check_params(eps, slope))) return rc;
+    if (!(momentum >= 0.f && momentum <= 1.f))
+        return fail(IABN_ERR_PARAM, "momentum must lie in [0, 1]");
+    if ((rc = check_workspace(N, C, HW, workspace, workspace_bytes))) return rc;
+    const bool vec = use_vector(HW, dtype, x_z, nullptr);
+    const Geom g = make_geom(N, C, HW, dtype, vec);
+    const FwdParams prm = {gamma, beta, running_mean, running_var, save_mean, save_var,
+                           nullptr, eps, momentum, slope};
+    launch_fwd_apply(dtype, vec, x_z, g, static_cast<const Partial*>(workspace), prm, true,
+                             kFwdInPlace, static_cast<hipStream_t>(stream));
+    return launched("fwd_apply");
+}
+
+int iabn_forward_train(void* x_z, int dtype, const float* gamma, const float* beta,
+                       float* running_mean, float* running_var, float* save_mean,
+                       float* save_var, float eps, float momentum, float slope, int64_t N,
+                       int64_t C, int64_t HW, void* workspace, size_t workspace_bytes,
+                       void* stream) {
+    return forward_train_impl(kFwdInPlace, x_z, nullptr, dtype, gamma, beta, running_mean,
+                              running_var, save_mean, save_var, eps, momentum, slope, N, C, HW,
+                              workspace, workspace_bytes, stream);
+}
+
+int iabn_forward_eval(void* x_z, int dtype, const float* gamma, const float* beta,
+                      const float* running_mean, const float* running_var, float eps,
+                      float slope, int64_t N, int64_t C, int64_t HW, void* stream) {
+    int rc = validate_common(dtype, N, C, HW, false);
+    if (rc) return rc;
+    if (empty(N, C, HW)) return ok();
+    if (!x_z || !gamma || !beta || !running_mean || !running_var)
+        return fail(IABN_ERR_NULL, "a tensor or parameter pointer is NULL");
+    if ((rc = check_params(eps, slope))) return rc;
+    const bool vec = use_vector(HW, dtype, x_z, nullptr);
+    const Geom g = make_geom(N, C, HW, dtype, vec);
+    const FwdParams prm = {gamma, beta, const_cast<float*>(running_mean),
+                           const_cast<float*>(running_var), nullptr, nullptr, nullptr, eps, 0.f,
+                           slope};
+    launch_fwd_apply(dtype, vec, x_z, g, static_cast<const Partial*>(nullptr), prm, false,
+                             kFwdInPlace, static_cast<hipStream_t>(stream));
+    return launched("fwd_eval");
+}
+
+int iabn_backward_reduce(const void* z, const void* dz, int dtype, const float* gamma,
+                         const float* beta, float slope, int64_t N, int64_t C, int64_t HW,
+                         void* workspace, size_t workspace_bytes, void* stream) {
+    int rc = validate_common(dtype, N, C, HW, true);
+    if (rc) return rc;
+    if (empty(N, C, HW)) return ok();
+    if (!z || !dz || !gamma || !beta)
+        return fail(IABN_ERR_NULL, "a tensor or parameter pointer is NULL");
+    if (!(slope > 0.f) || !std::isfinite(slope))
+        return fail(IABN_ERR_PARAM, "slope must be finite and > 0 (the activation must be invertible)");
+    if ((rc = check_workspace(N, C, HW, workspace, workspace_bytes))) return rc;
+    const bool vec = use_vector(HW, dtype, z, dz);
+    const Geom g = make_geom(N, C, HW, dtype, vec);
+    const BwdParams prm = {gamma, beta, nullptr, nullptr, nullptr, nullptr, 1.f, slope, 0};
+    launch_bwd_reduce(dtype, vec, z, static_cast<const void*>(nullptr), dz, g, prm,
+                              kBwdFromZ, static_cast<Partial*>(workspace),
+                              static_cast<hipStream_t>(stream));
+    return launched("bwd_reduce");
+}
+
+int iabn_backward_apply(const void* z, void* dz_dx, int dtype, const float* gamma,
+                        const float* beta, const float* save_var, float* dgamma, float* dbeta,
+                        float eps, float slope, int64_t N, int64_t C, int64_t HW,
+                        void* workspace, size_t workspace_bytes, void* stream) {
+    int rc = validate_common(dtype, N, C, HW, true);
+    if (rc) return rc;
+    if (empty(N, C, HW)) return ok();
+    if (!z || !dz_dx || !gamma || !beta || !save_var || !dgamma || !dbeta)
+        return fail(IABN_ERR_NULL, "a tensor or parameter pointer is NULL");
+    if ((rc = check_params(eps, slope))) return rc;
+    if ((rc = check_workspace(N, C, HW, workspace, workspace_bytes))) return rc;
+    const bool vec = use_vector(HW, dtype, z, dz_dx);
+    const Geom g = make_geom(N, C, HW, dtype, vec);
+    const BwdParams prm = {gamma, beta, nullptr, save_var, dgamma, dbeta, eps, slope, 0};
+    launch_bwd_apply(dtype, vec, z, static_cast<const void*>(nullptr), dz_dx, g,
+                             static_cast<const Partial*>(workspace), prm, kBwdFromZ,
+                             static_cast<hipStream_t>(stream));
+    return launched("bwd_apply");
+}
+
+int iabn_backward(const void* z, void* dz_dx, int dtype, const float* gamma, const float* beta,
+                  const float* save_var, float* dgamma, float* dbeta, float eps, float slope,
+                  int64_t N, int64_t C, int64_t HW, void* workspace, size_t workspace_bytes,
+                  void* stream) {
+    return backward_impl(kBwdFromZ, false, z, nullptr, dz_dx, dtype, gamma, beta, nullptr,
+                         save_var, dgamma, dbeta, eps, slope, N, C, HW, workspace,
+                         workspace_bytes, stream);
+}
+
+int iabn_backward_ii(const void* z, void* dz_dx, int dtype, const float* gamma,
+                     const float* beta, const float* save_var, float* dgamma, float* dbeta,
+                     float eps, float slope, int64_t N, int64_t C, int64_t HW, void* workspace,
+                     size_t workspace_bytes, void* stream) {
+    return backward_impl(kBwdFromZ, true, z, nullptr, dz_dx, dtype, gamma, beta, nullptr,
+                         save_var, dgamma, dbeta, eps, slope, N, C, HW, workspace,
+                         workspace_bytes, stream);
+}
+
+int iabn_std_forward_train(const void* x, void* z, int dtype, const float* gamma,
+                           const float* beta, float* running_mean, float* running_var,
+                           float* save_mean, float* save_var, float eps, float momentum,
+                           float slope, int64_t N, int64_t C, int64_t HW, void* workspace,
+                           size_t workspace_bytes, void* stream) {
+    return forward_train_impl(kFwdOut, const_cast<void*>(x), z, dtype, gamma, beta, running_mean,
+                              running_var, save_mean, save_var, eps, momentum, slope, N, C, HW,
+                              workspace, workspace_bytes, stream);
+}
+
+int iabn_std_backward(const void* x, const void* z, void* dz_dx, int dtype, const float* gamma,
+                      const float* beta, const float* save_mean, const float* save_var,
+                      float* dgamma, float* dbeta, float eps, float slope, int64_t N, int64_t C,
+                      int64_t HW, void* workspace, size_t workspace_bytes, void* stream) {
+    return backward_impl(kBwdFromXZ, false, x, z, dz_dx, dtype, gamma, beta, save_mean, save_var,
+                         dgamma, dbeta, eps, slope, N, C, HW, workspace, workspace_bytes, stream);
+}
+
+int iabn_ckpt_forward_train(void* x_xhat, void* z, int dtype, const float* gamma,
+                            const float* beta, float* running_mean, float* running_var,
+                            float* save_mean, float* save_var, float eps, float momentum,
+                            float slope, int64_t N, int64_t C, int64_t HW, void* workspace,
+                            size_t workspace_bytes, void* stream) {
+    return forward_train_impl(kFwdCkpt, x_xhat, z, dtype, gamma, beta, running_mean, running_var,
+                              save_mean, save_var, eps, momentum, slope, N, C, HW, workspace,
+                              workspace_bytes, stream);
+}
+
+int iabn_ckpt_recompute(const void* xhat, void* z, int dtype, const float* gamma,
+                        const float* beta, float slope, int64_t N, int64_t C, int64_t HW,
+                        void* stream) {
+    int rc = validate_common(dtype, N, C, HW, false);
+    if (rc) return rc;
+    if (empty(N, C, HW)) return ok();
+    if (!xhat || !z || !gamma || !beta)
+        return fail(IABN_ERR_NULL, "a tensor or parameter pointer is NULL");
+    if ((rc = check_params(1.f, slope))) return rc;
+    const bool vec = use_vector(HW, dtype, xhat, z);
+    const Geom g = make_geom(N, C, HW, dtype, vec);
+    launch_recompute(dtype, vec, xhat, z, g, gamma, beta, slope,
+                              static_cast<hipStream_t>(stream));
+    return launched("recompute");
+}
+
+int iabn_ckpt_backward(const void* xhat, void* dz_dx, int dtype, const float* gamma,
+                       const float* beta, const float* save_var, float* dgamma, float* dbeta,
+                       float eps, float slope, int64_t N, int64_t C, int64_t HW,
+                       void* workspace, size_t workspace_bytes, void* stream) {
+    return backward_impl(kBwdFromXhat, false, xhat, nullptr, dz_dx, dtype, gamma, beta, nullptr,
+                         save_var, dgamma, dbeta, eps, slope, N, C, HW, workspace,
+                         workspace_bytes, stream);
+}
+
+}  // extern "C"

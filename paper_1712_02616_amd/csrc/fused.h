@@ -1,0 +1,171 @@
+// Device helpers of the channel-resident (fused) kernels: raw 16-byte
+// registers, the block-level reductions of a channel, strip addressing, and
+// the optimiser barriers that keep the register-resident loops at their
+// register budget.
+#pragma once
+
+#include "common.h"
+
+namespace iabn_impl {
+
+// One block owns a whole channel and keeps the first R of each thread's
+// 16-byte accesses in registers between the reduction and the apply phase,
+// so those bytes cross HBM once on the way in and once on the way out (the
+// forward reads x and writes z; the backward reads z and dz and writes dx).
+// Accesses beyond R (channels larger than the block's registers) are read
+// again in the apply phase.  Thread t handles accesses t, t + T, t + 2T, ...
+// of its channel, so a wave touches consecutive 16-byte vectors.  The only
+// synchronisation is the block barrier around the channel's reduction.
+
+typedef uint32_t raw16_t __attribute__((ext_vector_type(4)));
+
+// Hide a value from the optimiser (an empty asm that "may change" it).  Used
+// after the reduction barrier so that the apply phase keeps only the raw
+// 16-byte registers alive and converts them again, instead of keeping the
+// twice-as-large fp32 values (and 64-bit addresses) from the first phase.
+template <typename V>
+__device__ __forceinline__ void opaque(V& v) {
+    asm volatile("" : "+v"(v));
+}
+
+// Keep the scheduler from interleaving the per-access steps of the register-
+// resident loops: interleaving them only raises register pressure (the loads
+// are already all in flight), and past the block's register budget it spills.
+__device__ __forceinline__ void sched_fence() { __builtin_amdgcn_sched_barrier(0); }
+
+template <int HINT>
+__device__ __forceinline__ raw16_t load_raw(const void* __restrict__ base, uint64_t idx) {
+    const raw16_t* p = static_cast<const raw16_t*>(base) + idx;
+    return HINT == kStream ? __builtin_nontemporal_load(p) : *p;
+}
+
+template <int DT, int VEC>
+__device__ __forceinline__ void unpack(raw16_t r, float (&v)[VEC]) {
+    using T = typename Elem<DT>::T;
+    typedef T vt __attribute__((ext_vector_type(VEC)));
+    typedef float vf __attribute__((ext_vector_type(VEC)));
+    const vf f = __builtin_convertvector(__builtin_bit_cast(vt, r), vf);
+#pragma unroll
+    for (int k = 0; k < VEC; ++k) v[k] = f[k];
+}
+
+// Per-wave (shift, s1, s2, n) of a block, combined by wave 0 in a fixed
+// order into the channel's mean and biased variance.
+template <int T>
+__device__ __forceinline__ void block_moments(float shift, float s1, float s2, uint32_t nacc,
+                                              uint32_t vec, double& mean, double& var) {
+    constexpr int W = T / kWave;
+    __shared__ double red[W][4];
+    __shared__ double out[2];
+    const double kw = __shfl(shift, 0, kWave);
+    const double n = static_cast<double>(nacc) * vec;
+    double d1 = s1, d2 = s2;
+    reshift(d1, d2, n, shift, kw);
+    d1 = wave_sum(d1);
+    d2 = wave_sum(d2);
+    const double nw = wave_sum(n);
+    const uint32_t wave = threadIdx.x / kWave;
+    if (lane_id() == 0) {
+        red[wave][0] = kw;
+        red[wave][1] = d1;
+        red[wave][2] = d2;
+        red[wave][3] = nw;
+    }
+    __syncthreads();
+    if (wave == 0) {
+        const double kref = red[0][0];
+        double t1 = 0.0, t2 = 0.0, tn = 0.0;
+        if (lane_id() < W) {
+            t1 = red[lane_id()][1];
+            t2 = red[lane_id()][2];
+            tn = red[lane_id()][3];
+            reshift(t1, t2, tn, red[lane_id()][0], kref);
+        }
+        t1 = wave_sum(t1);
+        t2 = wave_sum(t2);
+        tn = wave_sum(tn);
+        if (lane_id() == 0) {
+            out[0] = kref + t1 / tn;
+            out[1] = fmax(t2 - t1 * t1 / tn, 0.0) / tn;
+        }
+    }
+    __syncthreads();
+    mean = out[0];
+    var = out[1];
+}
+
+template <int T>
+__device__ __forceinline__ void block_sums(double a, double b, double& sa, double& sb) {
+    constexpr int W = T / kWave;
+    __shared__ double red[W][2];
+    __shared__ double out[2];
+    a = wave_sum(a);
+    b = wave_sum(b);
+    const uint32_t wave = threadIdx.x / kWave;
+    if (lane_id() == 0) {
+        red[wave][0] = a;
+        red[wave][1] = b;
+    }
+    __syncthreads();
+    if (wave == 0) {
+        double t1 = lane_id() < W ? red[lane_id()][0] : 0.0;
+        double t2 = lane_id() < W ? red[lane_id()][1] : 0.0;
+        t1 = wave_sum(t1);
+        t2 = wave_sum(t2);
+        if (lane_id() == 0) {
+            out[0] = t1;
+            out[1] = t2;
+        }
+    }
+    __syncthreads();
+    sa = out[0];
+    sb = out[1];
+}
+
+// Where each row of a channel holds a whole number of T-wide strips of
+// 16-byte accesses (vrow % T == 0) and the channel has at least R strips,
+// access k of every thread of the block lies in strip k: its index is a
+// block-uniform strip offset plus the thread index, and every thread has an
+// access in each of the vchan / T strips.  The strip offsets are scalar
+// (SGPR) arithmetic and the R resident accesses need no bounds test, so the
+// per-element path spends no vector instructions on addresses or bounds.
+// STRIP = false is the general mapping (row division per access, bounds per
+// lane).
+struct StripPos {
+    uint64_t off;  // index of the strip's first access
+    uint32_t col;  // column of the strip within its row
+};
+
+__device__ __forceinline__ StripPos strip_begin(const Geom& g, uint32_t c) {
+    StripPos s;
+    s.off = static_cast<uint64_t>(c) * g.vrow;
+    s.col = 0;
+    return s;
+}
+
+template <int T>
+__device__ __forceinline__ void strip_next(const Geom& g, StripPos& s) {
+    s.col += T;
+    s.off += T;
+    if (s.col == g.vrow) {
+        s.col = 0;
+        s.off += g.nstride - g.vrow;
+    }
+}
+
+// The same for a block-uniform strip position (kept in scalar registers):
+// the apply phase walks the strips again instead of keeping every strip
+// offset of the reduction phase alive.
+__device__ __forceinline__ void opaque_uniform(StripPos& s) {
+    asm volatile("" : "+s"(s.off), "+s"(s.col));
+}
+
+// The leaky ReLU as max(y, a*y) for a <= 1 and min(y, a*y) for a > 1: two
+// instructions, and the same value as the definition's branch (including
+// y = -0, which stays -0).
+template <bool SMALL_SLOPE>
+__device__ __forceinline__ float leaky(float y, float a) {
+    return SMALL_SLOPE ? fmaxf(y, a * y) : fminf(y, a * y);
+}
+
+}  // namespace iabn_impl

@@ -1,0 +1,288 @@
+// The channel-resident backward: one block per channel holds the stored
+// tensor(s) and dz in registers from the reduction to the apply, so each
+// crosses HBM once in and dx once out.  Formulations as in common.h
+// (InPlace-ABN I and II from z, standard from x and the signs of z,
+// checkpointing from xhat).
+
+#include "fused.h"
+#include "launch.h"
+
+namespace iabn_impl {
+namespace {
+
+// Backward of one channel per block (sums of dy and dy*w, dgamma, dbeta, dx
+// over dz), same arithmetic as bwd_reduce_kernel + bwd_apply_kernel.  u is z,
+// x or xhat (see BwdSign).  kBwdFromXZ reads the stored z as well but keeps
+// only its signs (one bit per element) for the apply phase.
+template <int DT, int VEC, int T, int R, bool STRIP, int BM>
+__device__ __forceinline__ void bwd_fused_channel(const void* __restrict__ u,
+                                                  const void* __restrict__ zs,
+                                                  void* __restrict__ dzdx, const Geom& g,
+                                                  const BwdParams& prm, uint32_t c) {
+    constexpr bool XZ = BM == kBwdFromXZ;
+    constexpr int NW = XZ ? (R * VEC + 31) / 32 : 1;
+    const uint64_t cbase = static_cast<uint64_t>(c) * g.vrow;
+    const uint32_t tid = threadIdx.x;
+    const uint32_t nstrips = STRIP ? g.vchan / T : 0;
+    // All per-channel inputs first: a load issued after the data loads would
+    // put another memory round trip after the reduction barrier.
+    const float gamma_c = prm.gamma[c], beta_c = prm.beta[c], var_c = prm.save_var[c];
+    const float mean_c = XZ ? prm.save_mean[c] : 0.f;
+    const double invstd =
+        1.0 / sqrt(static_cast<double>(var_c) + static_cast<double>(prm.eps));
+    const BwdReduceElem<BM> el =
+        make_reduce_elem<BM>(prm.slope, gamma_c, beta_c, mean_c, invstd, prm.ii != 0);
+
+    // Register-resident accesses non-temporal, the rest cached (see
+    // fwd_fused_channel).  kBwdFromXZ first loads z (into the registers x
+    // will use) and dz, turns z into sign bits, and only then loads x, so
+    // that no more than two tensors' worth of registers is live.
+    raw16_t ku[R], kg[R];
+    uint32_t negm[NW];
+#pragma unroll
+    for (int q = 0; q < NW; ++q) negm[q] = 0u;
+    auto resident_index = [&](int k, StripPos& p, bool& live) -> uint64_t {
+        if constexpr (STRIP) {
+            const uint64_t i = p.off + tid;
+            strip_next<T>(g, p);
+            live = true;
+            return i;
+        } else {
+            const uint32_t v = tid + k * T;
+            live = v < g.vchan;
+            return live ? access_index(g, cbase, v) : 0;
+        }
+    };
+    StripPos sp = strip_begin(g, c);
+    if constexpr (XZ) {
+        StripPos sz = sp;
+#pragma unroll
+        for (int k = 0; k < R; ++k) {
+            bool live;
+            const uint64_t i1 = resident_index(k, sz, live);
+            if (live) {
+                ku[k] = load_raw<kStream>(zs, i1);
+                kg[k] = load_raw<kStream>(dzdx, i1);
+            }
+        }
+#pragma unroll
+        for (int k = 0; k < R; ++k) {
+            if (STRIP || tid + k * T < g.vchan) {
+                float tz[VEC];
+                unpack<DT, VEC>(ku[k], tz);
+#pragma unroll
+                for (int e = 0; e < VEC; ++e)
+                    negm[(k * VEC + e) / 32] |= static_cast<uint32_t>(tz[e] < 0.f)
+                                                << ((k * VEC + e) % 32);
+            }
+        }
+        // The bits must exist before the x loads are issued (a memory clobber
+        // keeps the loads below this point and the bit arithmetic above it).
+#pragma unroll
+        for (int q = 0; q < NW; ++q) asm volatile("" : "+v"(negm[q])::"memory");
+#pragma unroll
+        for (int k = 0; k < R; ++k) {
+            bool live;
+            const uint64_t i1 = resident_index(k, sp, live);
+            if (live) ku[k] = load_raw<kStream>(u, i1);
+        }
+    } else {
+#pragma unroll
+        for (int k = 0; k < R; ++k) {
+            bool live;
+            const uint64_t i1 = resident_index(k, sp, live);
+            if (live) {
+                ku[k] = load_raw<kStream>(u, i1);
+                kg[k] = load_raw<kStream>(dzdx, i1);
+            }
+        }
+    }
+    // fp32 within one access, fp64 across accesses (as the streaming reduce
+    // does per unrolled step): a channel's sums of dy cancel to near zero and
+    // an fp32 running sum over the whole register-resident part loses that.
+    double acc_dy = 0.0, acc_dyw = 0.0;
+#pragma unroll
+    for (int k = 0; k < R; ++k) {
+        if (STRIP || tid + k * T < g.vchan) {
+            float tu[VEC], tg[VEC];
+            unpack<DT, VEC>(ku[k], tu);
+            unpack<DT, VEC>(kg[k], tg);
+            float sdy = 0.f, sdyw = 0.f;
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) {
+                float dy, w;
+                if constexpr (XZ) {
+                    const bool neg = (negm[(k * VEC + e) / 32] >> ((k * VEC + e) % 32)) & 1u;
+                    el.with_neg(neg, tu[e], tg[e], dy, w);
+                } else {
+                    el(tu[e], 0.f, tg[e], dy, w);
+                }
+                sdy += dy;
+                sdyw = fmaf(dy, w, sdyw);
+            }
+            acc_dy += sdy;
+            acc_dyw += sdyw;
+        }
+        sched_fence();
+    }
+    auto accumulate = [&](uint64_t i1) {
+        float tu[VEC], tz[VEC], tg[VEC];
+        unpack<DT, VEC>(load_raw<kCached>(u, i1), tu);
+        if constexpr (XZ) unpack<DT, VEC>(load_raw<kCached>(zs, i1), tz);
+        else
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) tz[e] = 0.f;
+        unpack<DT, VEC>(load_raw<kCached>(dzdx, i1), tg);
+        float sdy = 0.f, sdyw = 0.f;
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) {
+            float dy, w;
+            el(tu[e], tz[e], tg[e], dy, w);
+            sdy += dy;
+            sdyw = fmaf(dy, w, sdyw);
+        }
+        acc_dy += sdy;
+        acc_dyw += sdyw;
+    };
+    if constexpr (STRIP) {
+#pragma unroll 1
+        for (uint32_t k = R; k < nstrips; ++k) {
+            accumulate(sp.off + tid);
+            strip_next<T>(g, sp);
+        }
+    } else {
+#pragma unroll 1
+        for (uint32_t v = tid + R * T; v < g.vchan; v += T) accumulate(access_index(g, cbase, v));
+    }
+
+    double dbeta, sdyw;
+    block_sums<T>(acc_dy, acc_dyw, dbeta, sdyw);
+    uint32_t tid2 = tid;
+    opaque(tid2);
+#pragma unroll
+    for (int k = 0; k < R; ++k) {
+        opaque(ku[k]);
+        opaque(kg[k]);
+    }
+#pragma unroll
+    for (int q = 0; q < NW; ++q) opaque(negm[q]);
+    const double A = static_cast<double>(gamma_c) * invstd;
+    const BwdApplyElem<BM> dx_of = make_apply_elem<BM>(A, sdyw, dbeta, g.m, prm.slope, gamma_c,
+                                                       beta_c, mean_c, invstd, prm.ii != 0);
+    if (tid == 0) {
+        prm.dgamma[c] = static_cast<float>(sdyw);
+        prm.dbeta[c] = static_cast<float>(dbeta);
+    }
+    auto emit = [&](raw16_t ru, raw16_t rz, raw16_t rg, uint64_t idx) {
+        float tu[VEC], tz[VEC], tg[VEC];
+        unpack<DT, VEC>(ru, tu);
+        if constexpr (XZ) unpack<DT, VEC>(rz, tz);
+        else
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) tz[e] = 0.f;
+        unpack<DT, VEC>(rg, tg);
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) tg[e] = dx_of(tu[e], tz[e], tg[e]);
+        store_vec<DT, VEC, kHintBwdApplyStore>(dzdx, idx, tg);
+    };
+    // The resident accesses: dx from registers (kBwdFromXZ: signs from the bits).
+    StripPos sq = strip_begin(g, c);
+#pragma unroll
+    for (int k = 0; k < R; ++k) {
+        uint64_t idx = 0;
+        bool live = true;
+        if constexpr (STRIP) {
+            idx = sq.off + tid2;
+            strip_next<T>(g, sq);
+        } else {
+            const uint32_t v = tid2 + k * T;
+            live = v < g.vchan;
+            if (live) idx = access_index(g, cbase, v);
+        }
+        if (live) {
+            float tu[VEC], tg[VEC];
+            unpack<DT, VEC>(ku[k], tu);
+            unpack<DT, VEC>(kg[k], tg);
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) {
+                if constexpr (XZ) {
+                    const bool neg = (negm[(k * VEC + e) / 32] >> ((k * VEC + e) % 32)) & 1u;
+                    tg[e] = dx_of.with_neg(neg, tu[e], tg[e]);
+                } else {
+                    tg[e] = dx_of(tu[e], 0.f, tg[e]);
+                }
+            }
+            store_vec<DT, VEC, kHintBwdApplyStore>(dzdx, idx, tg);
+        }
+        sched_fence();
+    }
+    const raw16_t zero16 = {0u, 0u, 0u, 0u};
+    if constexpr (STRIP) {
+#pragma unroll 1
+        for (uint32_t k = R; k < nstrips; ++k) {
+            const uint64_t i1 = sq.off + tid2;
+            emit(load_raw<kStream>(u, i1), XZ ? load_raw<kStream>(zs, i1) : zero16,
+                 load_raw<kStream>(dzdx, i1), i1);
+            strip_next<T>(g, sq);
+        }
+    } else {
+#pragma unroll 1
+        for (uint32_t v = tid2 + R * T; v < g.vchan; v += T) {
+            const uint64_t i1 = access_index(g, cbase, v);
+            emit(load_raw<kStream>(u, i1), XZ ? load_raw<kStream>(zs, i1) : zero16,
+                 load_raw<kStream>(dzdx, i1), i1);
+        }
+    }
+}
+
+template <int DT, int VEC, int T, int R, bool STRIP, int BM>
+__global__ __launch_bounds__(T) void bwd_fused_kernel(const void* __restrict__ u,
+                                                      const void* __restrict__ zs,
+                                                      void* __restrict__ dzdx, Geom g,
+                                                      BwdParams prm) {
+    bwd_fused_channel<DT, VEC, T, R, STRIP, BM>(u, zs, dzdx, g, prm, blockIdx.x);
+}
+
+#define IABN_FUSED_CASE(KERNEL, MODE, TT, RR, ...)                                             \
+    if (fp.T == TT && fp.R == RR) {                                                           \
+        if (kUseStrips && g.vrow % TT == 0 && g.vchan / TT >= RR)                             \
+            KERNEL<DT, V, TT, RR, true, MODE><<<grid, TT, lds, st>>>(__VA_ARGS__);            \
+        else                                                                                  \
+            KERNEL<DT, V, TT, RR, false, MODE><<<grid, TT, lds, st>>>(__VA_ARGS__);           \
+        return true;                                                                          \
+    }
+
+template <int DT, int BM>
+bool launch_bwd_fused(const void* u, const void* zs, void* dzdx, const Geom& g,
+                      const FusedPlan& fp, const BwdParams& prm, hipStream_t st) {
+    constexpr int V = 16 / sizeof(typename Elem<DT>::T);
+    const dim3 grid = fused_grid(g, fp);
+    const size_t lds = fused_lds(kFusedBwdBlocksPerCU);
+    IABN_FUSED_CASE(bwd_fused_kernel, BM, 256, 4, u, zs, dzdx, g, prm)
+    IABN_FUSED_CASE(bwd_fused_kernel, BM, 512, 4, u, zs, dzdx, g, prm)
+    IABN_FUSED_CASE(bwd_fused_kernel, BM, 256, 16, u, zs, dzdx, g, prm)
+    IABN_FUSED_CASE(bwd_fused_kernel, BM, 512, 16, u, zs, dzdx, g, prm)
+    IABN_FUSED_CASE(bwd_fused_kernel, BM, 1024, 8, u, zs, dzdx, g, prm)
+    return false;
+}
+
+#undef IABN_FUSED_CASE
+
+template <int BM>
+bool launch_dt(int dtype, const void* u, const void* zs, void* dzdx, const Geom& g,
+               const FusedPlan& fp, const BwdParams& prm, hipStream_t st) {
+    return dtype == IABN_F32   ? launch_bwd_fused<IABN_F32, BM>(u, zs, dzdx, g, fp, prm, st)
+           : dtype == IABN_F16 ? launch_bwd_fused<IABN_F16, BM>(u, zs, dzdx, g, fp, prm, st)
+                               : launch_bwd_fused<IABN_BF16, BM>(u, zs, dzdx, g, fp, prm, st);
+}
+
+}  // namespace
+
+bool launch_bwd_fused(int dtype, int bm, const void* u, const void* zs, void* dzdx, const Geom& g,
+                      const FusedPlan& fp, const BwdParams& prm, hipStream_t st) {
+    return bm == kBwdFromXZ     ? launch_dt<kBwdFromXZ>(dtype, u, zs, dzdx, g, fp, prm, st)
+           : bm == kBwdFromXhat ? launch_dt<kBwdFromXhat>(dtype, u, zs, dzdx, g, fp, prm, st)
+                                : launch_dt<kBwdFromZ>(dtype, u, zs, dzdx, g, fp, prm, st);
+}
+
+}  // namespace iabn_impl

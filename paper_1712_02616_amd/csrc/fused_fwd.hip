@@ -1,0 +1,262 @@
+// The channel-resident training forward: one block per channel holds the
+// channel's 16-byte accesses in registers from the statistics to the apply,
+// so x crosses HBM once in and the outputs once out.  Output modes as in
+// common.h (InPlace-ABN, standard, checkpointing).
+
+#include "fused.h"
+#include "launch.h"
+
+namespace iabn_impl {
+namespace {
+
+// Per-channel constants of the fused forward's apply phase.
+struct FwdApplyK {
+    float mean_hi, scale, bshift, slope;  // y = (x - mean_hi) * scale + bshift (kFwdCkpt: xhat)
+    float gamma, beta;                    // kFwdCkpt: y = gamma * xhat + beta
+    void* out;                            // kFwdOut / kFwdCkpt: z
+};
+
+// The outputs of one 16-byte access from its input values t (overwritten).
+template <int DT, int VEC, int FM, bool SMALL_SLOPE>
+__device__ __forceinline__ void fwd_fused_emit(void* __restrict__ xz, uint64_t idx,
+                                               float (&t)[VEC], const FwdApplyK& k) {
+    if constexpr (FM == kFwdCkpt) {
+        float zv[VEC];
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) {
+            t[e] = storage_round<DT>(fmaf(t[e] - k.mean_hi, k.scale, k.bshift));
+            zv[e] = leaky<SMALL_SLOPE>(fmaf(t[e], k.gamma, k.beta), k.slope);
+        }
+        store_vec<DT, VEC, kHintFwdApplyStore>(xz, idx, t);
+        store_vec<DT, VEC, kHintFwdApplyStore>(k.out, idx, zv);
+    } else {
+#pragma unroll
+        for (int e = 0; e < VEC; ++e)
+            t[e] = leaky<SMALL_SLOPE>(fmaf(t[e] - k.mean_hi, k.scale, k.bshift), k.slope);
+        store_vec<DT, VEC, kHintFwdApplyStore>(FM == kFwdOut ? k.out : xz, idx, t);
+    }
+}
+
+// Apply phase of the fused forward for the thread's resident accesses (from
+// registers) and the remainder (loaded again).
+template <int DT, int VEC, int T, int R, bool STRIP, int FM, bool SMALL_SLOPE>
+__device__ __forceinline__ void fwd_fused_apply(void* __restrict__ xz, const Geom& g, uint32_t c,
+                                                uint32_t tid, const raw16_t (&keep)[R],
+                                                const FwdApplyK& kk) {
+    const uint64_t cbase = static_cast<uint64_t>(c) * g.vrow;
+    const uint32_t nstrips = STRIP ? g.vchan / T : 0;
+    StripPos sq = strip_begin(g, c);
+    opaque_uniform(sq);
+#pragma unroll
+    for (int k = 0; k < R; ++k) {
+        uint64_t idx = 0;
+        bool live = true;
+        if constexpr (STRIP) {
+            idx = sq.off + tid;
+            strip_next<T>(g, sq);
+        } else {
+            const uint32_t v = tid + k * T;
+            live = v < g.vchan;
+            if (live) idx = access_index(g, cbase, v);
+        }
+        if (live) {
+            float t[VEC];
+            unpack<DT, VEC>(keep[k], t);
+            fwd_fused_emit<DT, VEC, FM, SMALL_SLOPE>(xz, idx, t, kk);
+        }
+        sched_fence();
+    }
+    if constexpr (STRIP) {
+#pragma unroll 1
+        for (uint32_t k = R; k < nstrips; ++k) {
+            const uint64_t idx = sq.off + tid;
+            float t[VEC];
+            unpack<DT, VEC>(load_raw<kStream>(xz, idx), t);
+            fwd_fused_emit<DT, VEC, FM, SMALL_SLOPE>(xz, idx, t, kk);
+            strip_next<T>(g, sq);
+        }
+    } else {
+#pragma unroll 1
+        for (uint32_t v = tid + R * T; v < g.vchan; v += T) {
+            const uint64_t idx = access_index(g, cbase, v);
+            float t[VEC];
+            unpack<DT, VEC>(load_raw<kStream>(xz, idx), t);
+            fwd_fused_emit<DT, VEC, FM, SMALL_SLOPE>(xz, idx, t, kk);
+        }
+    }
+}
+
+// Training forward of one channel per block (statistics, running estimates,
+// z over x), same arithmetic as fwd_stats_kernel + fwd_apply_kernel.
+template <int DT, int VEC, int T, int R, bool STRIP, int FM>
+__device__ __forceinline__ void fwd_fused_channel(void* __restrict__ xz, const Geom& g,
+                                                  const FwdParams& prm, uint32_t c) {
+    const uint64_t cbase = static_cast<uint64_t>(c) * g.vrow;
+    const uint32_t tid = threadIdx.x;
+    const uint32_t nstrips = STRIP ? g.vchan / T : 0;
+    raw16_t* const xv = static_cast<raw16_t*>(xz);
+    // Per-channel inputs before the data loads (see bwd_fused_channel).
+    const float gamma_c = prm.gamma[c], beta_c = prm.beta[c];
+    float rm_c = 0.f, rv_c = 0.f;
+    if (tid == 0) {
+        rm_c = prm.running_mean[c];
+        rv_c = prm.running_var[c];
+    }
+
+    // The first R accesses per thread stay in registers until the apply, so
+    // this is their only read: non-temporal.  Accesses past those are read
+    // again by the apply and go through the caches.  (Measured: non-temporal
+    // register-resident loads cut the forward over the backbone sweep by 12%
+    // and the backward by 7%.)
+    raw16_t keep[R];
+    StripPos sp = strip_begin(g, c);
+#pragma unroll
+    for (int k = 0; k < R; ++k) {
+        if constexpr (STRIP) {
+            keep[k] = load_raw<kStream>(xv, sp.off + tid);
+            strip_next<T>(g, sp);
+        } else {
+            const uint32_t v = tid + k * T;
+            if (v < g.vchan) keep[k] = load_raw<kStream>(xz, access_index(g, cbase, v));
+        }
+    }
+    float shift = 0.f, s1 = 0.f, s2 = 0.f;
+    uint32_t nacc = 0;
+    if (tid < g.vchan) {
+        float t[VEC];
+        unpack<DT, VEC>(keep[0], t);
+        shift = t[0];
+    }
+    auto accumulate = [&](raw16_t r) {
+        float t[VEC];
+        unpack<DT, VEC>(r, t);
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) {
+            const float d = t[e] - shift;
+            s1 += d;
+            s2 = fmaf(d, d, s2);
+        }
+        ++nacc;
+    };
+#pragma unroll
+    for (int k = 0; k < R; ++k) {
+        if (STRIP || tid + k * T < g.vchan) {
+            float t[VEC];
+            unpack<DT, VEC>(keep[k], t);
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) {
+                const float d = t[e] - shift;
+                s1 += d;
+                s2 = fmaf(d, d, s2);
+            }
+            ++nacc;
+        }
+        sched_fence();
+    }
+    if constexpr (STRIP) {
+#pragma unroll 1
+        for (uint32_t k = R; k < nstrips; ++k) {
+            accumulate((xv + sp.off)[tid]);
+            strip_next<T>(g, sp);
+        }
+    } else {
+#pragma unroll 1
+        for (uint32_t v = tid + R * T; v < g.vchan; v += T)
+            accumulate(load_raw<kCached>(xz, access_index(g, cbase, v)));
+    }
+
+    double mean, var;
+    block_moments<T>(shift, s1, s2, nacc, VEC, mean, var);
+    uint32_t tid2 = tid;
+    opaque(tid2);
+#pragma unroll
+    for (int k = 0; k < R; ++k) opaque(keep[k]);
+    const double invstd = 1.0 / sqrt(var + static_cast<double>(prm.eps));
+    const double scale_d = FM == kFwdCkpt ? invstd : static_cast<double>(gamma_c) * invstd;
+    const float mean_hi = static_cast<float>(mean);
+    const double mean_lo = mean - static_cast<double>(mean_hi);
+    // (x - mu) * scale + beta with mu = mean_hi + mean_lo: the low part goes
+    // into the shift (kFwdCkpt: beta comes after the rounding of xhat).
+    FwdApplyK kk;
+    kk.mean_hi = mean_hi;
+    kk.scale = static_cast<float>(scale_d);
+    kk.bshift = static_cast<float>((FM == kFwdCkpt ? 0.0 : static_cast<double>(beta_c)) -
+                                   mean_lo * scale_d);
+    kk.slope = prm.slope;
+    kk.gamma = gamma_c;
+    kk.beta = beta_c;
+    kk.out = prm.out;
+    if (tid == 0) {
+        const double mom = prm.momentum;
+        const double m = g.m;
+        prm.save_mean[c] = mean_hi;
+        prm.save_var[c] = static_cast<float>(var);
+        prm.running_mean[c] = static_cast<float>((1.0 - mom) * static_cast<double>(rm_c) + mom * mean);
+        prm.running_var[c] = static_cast<float>((1.0 - mom) * static_cast<double>(rv_c) +
+                                                mom * var * (m / (m - 1.0)));
+    }
+
+    if (kk.slope <= 1.f)
+        fwd_fused_apply<DT, VEC, T, R, STRIP, FM, true>(xz, g, c, tid2, keep, kk);
+    else
+        fwd_fused_apply<DT, VEC, T, R, STRIP, FM, false>(xz, g, c, tid2, keep, kk);
+}
+
+// One block per channel: c = blockIdx.x.  (Giving each XCD a contiguous
+// range of channels, rather than every eighth channel as the round-robin
+// hand-out of workgroups to the 8 XCDs does, was measured 4% slower.  Blocks
+// that loop over several
+// channels were measured slower, both plainly and with the next channel
+// prefetched into a second register buffer: the second buffer limits a CU to
+// one block, and at that occupancy the per-channel reduce-barrier-apply chain
+// costs more than the overlap of one channel's stores with the next one's
+// loads gains.)
+template <int DT, int VEC, int T, int R, bool STRIP, int FM>
+__global__ __launch_bounds__(T) void fwd_fused_kernel(void* __restrict__ xz, Geom g,
+                                                      FwdParams prm) {
+    fwd_fused_channel<DT, VEC, T, R, STRIP, FM>(xz, g, prm, blockIdx.x);
+}
+
+#define IABN_FUSED_CASE(KERNEL, MODE, TT, RR, ...)                                             \
+    if (fp.T == TT && fp.R == RR) {                                                           \
+        if (kUseStrips && g.vrow % TT == 0 && g.vchan / TT >= RR)                             \
+            KERNEL<DT, V, TT, RR, true, MODE><<<grid, TT, lds, st>>>(__VA_ARGS__);            \
+        else                                                                                  \
+            KERNEL<DT, V, TT, RR, false, MODE><<<grid, TT, lds, st>>>(__VA_ARGS__);           \
+        return true;                                                                          \
+    }
+
+template <int DT, int FM>
+bool launch_fwd_fused(void* xz, const Geom& g, const FusedPlan& fp, const FwdParams& prm,
+                      hipStream_t st) {
+    constexpr int V = 16 / sizeof(typename Elem<DT>::T);
+    const dim3 grid = fused_grid(g, fp);
+    const size_t lds = fused_lds(kFusedFwdBlocksPerCU);
+    IABN_FUSED_CASE(fwd_fused_kernel, FM, 256, 4, xz, g, prm)
+    IABN_FUSED_CASE(fwd_fused_kernel, FM, 512, 4, xz, g, prm)
+    IABN_FUSED_CASE(fwd_fused_kernel, FM, 256, 16, xz, g, prm)
+    IABN_FUSED_CASE(fwd_fused_kernel, FM, 512, 16, xz, g, prm)
+    IABN_FUSED_CASE(fwd_fused_kernel, FM, 1024, 16, xz, g, prm)
+    return false;
+}
+
+#undef IABN_FUSED_CASE
+
+template <int FM>
+bool launch_dt(int dtype, void* xz, const Geom& g, const FusedPlan& fp, const FwdParams& prm,
+               hipStream_t st) {
+    return dtype == IABN_F32   ? launch_fwd_fused<IABN_F32, FM>(xz, g, fp, prm, st)
+           : dtype == IABN_F16 ? launch_fwd_fused<IABN_F16, FM>(xz, g, fp, prm, st)
+                               : launch_fwd_fused<IABN_BF16, FM>(xz, g, fp, prm, st);
+}
+
+}  // namespace
+
+bool launch_fwd_fused(int dtype, int fm, void* xz, const Geom& g, const FusedPlan& fp,
+                      const FwdParams& prm, hipStream_t st) {
+    return fm == kFwdOut    ? launch_dt<kFwdOut>(dtype, xz, g, fp, prm, st)
+           : fm == kFwdCkpt ? launch_dt<kFwdCkpt>(dtype, xz, g, fp, prm, st)
+                            : launch_dt<kFwdInPlace>(dtype, xz, g, fp, prm, st);
+}
+
+}  // namespace iabn_impl

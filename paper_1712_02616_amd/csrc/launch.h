@@ -1,0 +1,86 @@
+// Host-side launchers of libiabn's kernels, one per kernel family, and the
+// planning of the channel-resident (fused) kernels.  Each launcher picks the
+// template instance for the storage type, access width and mode and enqueues
+// it on the stream; it neither validates (the C ABI in api.hip does that
+// before any launch) nor reports launch errors (the caller reads
+// hipGetLastError).
+#pragma once
+
+#include "common.h"
+
+namespace iabn_impl {
+
+// ---- streaming kernels (stream.hip)
+
+void launch_fwd_stats(int dtype, bool vec, const void* x, const Geom& g, Partial* part,
+                      hipStream_t st);
+// train = false is inference (in place); otherwise fm is the output mode.
+void launch_fwd_apply(int dtype, bool vec, void* xz, const Geom& g, const Partial* part,
+                      const FwdParams& prm, bool train, int fm, hipStream_t st);
+void launch_bwd_reduce(int dtype, bool vec, const void* u, const void* zs, const void* dz,
+                       const Geom& g, const BwdParams& prm, int bm, Partial* part, hipStream_t st);
+void launch_bwd_apply(int dtype, bool vec, const void* u, const void* zs, void* dzdx,
+                      const Geom& g, const Partial* part, const BwdParams& prm, int bm,
+                      hipStream_t st);
+void launch_recompute(int dtype, bool vec, const void* xhat, void* z, const Geom& g,
+                      const float* gamma, const float* beta, float slope, hipStream_t st);
+
+// ---- channel-resident kernels (fused_fwd.hip, fused_bwd.hip)
+
+// Used when every channel gets a block of its own and at least one block per
+// CU (C >= kFusedMinChannels) on the 16-byte path.
+constexpr int64_t kFusedMinChannels = 256;
+
+struct FusedPlan {
+    int T;  // threads per block
+    int R;  // 16-byte accesses per thread held in registers (per tensor)
+};
+
+inline dim3 fused_grid(const Geom& g, const FusedPlan&) { return dim3(g.C); }
+
+// Resident blocks per CU of a fused launch (0: as many as registers allow).
+// Fewer resident blocks run the channels in several rounds, so the loads of
+// a later round overlap the stores of an earlier one instead of every block
+// reading, then every block writing.  The cap is applied by reserving LDS.
+constexpr int kFusedFwdBlocksPerCU = 0;
+constexpr int kFusedBwdBlocksPerCU = 0;
+constexpr size_t kLdsPerCU = 160 * 1024;
+
+inline size_t fused_lds(int blocks_per_cu) {
+    if (blocks_per_cu <= 0) return 0;
+    return kLdsPerCU / blocks_per_cu - 2048;  // leaves room for the kernels' own reduction buffers
+}
+
+// Candidate (T, R) in order of preference (each one has a kernel built in
+// launch_fwd_fused / launch_bwd_fused): the first whose threads hold the
+// whole channel is used; larger channels take the last entry and re-read
+// the remainder.  The backward holds two tensors, so its largest blocks keep
+// half as many accesses per thread.
+// Fused kernels use strip addressing where the shape allows it.
+constexpr bool kUseStrips = true;
+
+constexpr FusedPlan kFwdLadder[] = {{256, 4}, {512, 4}, {256, 16}, {512, 16}, {1024, 16}};
+constexpr FusedPlan kBwdLadder[] = {{256, 4}, {512, 4}, {256, 16}, {512, 16}, {1024, 8}};
+
+inline bool plan_fused(int64_t C, const Geom& g, bool vector, bool backward, FusedPlan* out) {
+    if (!vector || C < kFusedMinChannels) return false;
+    const int64_t A = g.vchan;
+    const FusedPlan* ladder = backward ? kBwdLadder : kFwdLadder;
+    const int n = backward ? int(sizeof kBwdLadder / sizeof kBwdLadder[0])
+                           : int(sizeof kFwdLadder / sizeof kFwdLadder[0]);
+    for (int i = 0; i < n; ++i) {
+        if (A <= static_cast<int64_t>(ladder[i].T) * ladder[i].R || i == n - 1) {
+            *out = ladder[i];
+            return true;
+        }
+    }
+    return false;
+}
+
+// False if no kernel is built for the plan's (T, R) (a planning bug).
+bool launch_fwd_fused(int dtype, int fm, void* xz, const Geom& g, const FusedPlan& fp,
+                      const FwdParams& prm, hipStream_t st);
+bool launch_bwd_fused(int dtype, int bm, const void* u, const void* zs, void* dzdx, const Geom& g,
+                      const FusedPlan& fp, const BwdParams& prm, hipStream_t st);
+
+}  // namespace iabn_impl
