@@ -262,7 +262,7 @@ bool launch_bwd_fused(const void* u, const void* zs, void* dzdx, const Geom& g,
     IABN_FUSED_CASE(bwd_fused_kernel, BM, 512, 4, u, zs, dzdx, g, prm)
     IABN_FUSED_CASE(bwd_fused_kernel, BM, 256, 16, u, zs, dzdx, g, prm)
     IABN_FUSED_CASE(bwd_fused_kernel, BM, 512, 16, u, zs, dzdx, g, prm)
-    IABN_FUSED_CASE(bwd_fused_kernel, BM, 1024, 8, u, zs, dzdx, g, prm)
+    IABN_FUSED_CASE(bwd_fused_kernel, BM, 1024, 11, u, zs, dzdx, g, prm)
     return false;
 }
 
