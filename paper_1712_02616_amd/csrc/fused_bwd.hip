@@ -11,9 +11,10 @@ namespace iabn_impl {
 namespace {
 
 // Backward of one channel per block (sums of dy and dy*w, dgamma, dbeta, dx
-// over dz), same arithmetic as bwd_reduce_kernel + bwd_apply_kernel.  u is z,
-// x or xhat (see BwdSign).  kBwdFromXZ reads the stored z as well but keeps
-// only its signs (one bit per element) for the apply phase.
+// over dz), same arithmetic as bwd_reduce_kernel + bwd_apply_kernel in
+// stream.hip.  u is z, x or xhat (see BwdSign).  kBwdFromXZ reads the stored
+// z as well but keeps only its signs (one bit per element) for the apply
+// phase.
 template <int DT, int VEC, int T, int R, bool STRIP, int BM>
 __device__ __forceinline__ void bwd_fused_channel(const void* __restrict__ u,
                                                   const void* __restrict__ zs,
@@ -235,6 +236,7 @@ __device__ __forceinline__ void bwd_fused_channel(const void* __restrict__ u,
     }
 }
 
+// One block per channel: c = blockIdx.x (see fwd_fused_kernel).
 template <int DT, int VEC, int T, int R, bool STRIP, int BM>
 __global__ __launch_bounds__(T) void bwd_fused_kernel(const void* __restrict__ u,
                                                       const void* __restrict__ zs,

@@ -87,7 +87,8 @@ __device__ __forceinline__ void fwd_fused_apply(void* __restrict__ xz, const Geo
 }
 
 // Training forward of one channel per block (statistics, running estimates,
-// z over x), same arithmetic as fwd_stats_kernel + fwd_apply_kernel.
+// z over x), same arithmetic as fwd_stats_kernel + fwd_apply_kernel in
+// stream.hip.
 template <int DT, int VEC, int T, int R, bool STRIP, int FM>
 __device__ __forceinline__ void fwd_fused_channel(void* __restrict__ xz, const Geom& g,
                                                   const FwdParams& prm, uint32_t c) {
@@ -205,12 +206,11 @@ __device__ __forceinline__ void fwd_fused_channel(void* __restrict__ xz, const G
 // One block per channel: c = blockIdx.x.  (Giving each XCD a contiguous
 // range of channels, rather than every eighth channel as the round-robin
 // hand-out of workgroups to the 8 XCDs does, was measured 4% slower.  Blocks
-// that loop over several
-// channels were measured slower, both plainly and with the next channel
-// prefetched into a second register buffer: the second buffer limits a CU to
-// one block, and at that occupancy the per-channel reduce-barrier-apply chain
-// costs more than the overlap of one channel's stores with the next one's
-// loads gains.)
+// that loop over several channels were measured slower, both plainly and
+// with the next channel prefetched into a second register buffer: the second
+// buffer limits a CU to one block, and at that occupancy the per-channel
+// reduce-barrier-apply chain costs more than the overlap of one channel's
+// stores with the next one's loads gains.)
 template <int DT, int VEC, int T, int R, bool STRIP, int FM>
 __global__ __launch_bounds__(T) void fwd_fused_kernel(void* __restrict__ xz, Geom g,
                                                       FwdParams prm) {
