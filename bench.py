@@ -227,7 +227,7 @@ def time_arms(lib, layers, refresh, check, stream, args, E_total, b, iabn_kernel
 def main():
     args = parse()
     if args.gpus != 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path "
+        print("bench.py measures one GPU only: the library has no multi-GPU path "
               "(got --gpus %d)" % args.gpus, file=sys.stderr)
         sys.exit(2)
     if os.environ.get("WORLD_SIZE", "1") != "1":
