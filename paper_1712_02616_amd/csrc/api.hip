@@ -83,14 +83,11 @@ size_t workspace_bytes_for(int64_t N, int64_t C, int64_t HW) {
     return static_cast<size_t>(C) * static_cast<size_t>(sp.P) * kWaves * sizeof(Partial);
 }
 
-bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
-// The access geometry.  vector=true uses 16-byte accesses (requires
-// HW % (16/elem) == 0 and 16-byte aligned pointers).
-Geom make_geom(int64_t N, int64_t C, int64_t HW, int dtype, bool vector) {
+// The access geometry for `vec` elements per access.
+Geom make_geom(int64_t N, int64_t C, int64_t HW, int dtype, int vec) {
     const int64_t m = N * HW;
     const Split sp = split_channel(m, C);
-    const int64_t vec = vector ? 16 / elem_bytes(dtype) : 1;
     Geom g;
     g.C = static_cast<uint32_t>(C);
     g.P = static_cast<uint32_t>(sp.P);
@@ -104,9 +101,22 @@ Geom make_geom(int64_t N, int64_t C, int64_t HW, int dtype, bool vector) {
     return g;
 }
 
-bool use_vector(int64_t HW, int dtype, const void* a, const void* b) {
-    const int64_t vec = 16 / elem_bytes(dtype);
-    return HW % vec == 0 && aligned16(a) && (b == nullptr || aligned16(b));
+bool aligned_to(const void* p, uintptr_t bytes) {
+    return p == nullptr || (reinterpret_cast<uintptr_t>(p) & (bytes - 1)) == 0;
+}
+
+// Elements per access: the widest of 16, 8, 4 (and 2 for 2-byte types)
+// bytes that divides a row and to which every given tensor is aligned (an
+// access never crosses a row; slices start on multiples of 8 elements, so
+// every width divides them).  Null pointers are ignored.
+int access_vec(int64_t HW, int dtype, const void* a, const void* b, const void* c) {
+    const int eb = elem_bytes(dtype);
+    for (int bytes = 16; bytes > eb; bytes /= 2) {
+        const int v = bytes / eb;
+        if (HW % v == 0 && aligned_to(a, bytes) && aligned_to(b, bytes) && aligned_to(c, bytes))
+            return v;
+    }
+    return 1;
 }
 
 int check_workspace(int64_t N, int64_t C, int64_t HW, const void* ws, size_t bytes) {
@@ -140,10 +150,6 @@ int validate_common(int dtype, int64_t N, int64_t C, int64_t HW, bool train) {
 
 bool empty(int64_t N, int64_t C, int64_t HW) { return C == 0 || N * HW == 0; }
 
-bool vector_ok(int64_t HW, int dtype, const void* a, const void* b, const void* c) {
-    return use_vector(HW, dtype, a, b) && (c == nullptr || aligned16(c));
-}
-
 const char* fwd_name(int fm) {
     return fm == kFwdOut ? "standard forward" : fm == kFwdCkpt ? "checkpointing forward" : "forward";
 }
@@ -167,13 +173,13 @@ int forward_train_impl(int fm, void* x, void* out, int dtype, const float* gamma
     if (!(momentum >= 0.f && momentum <= 1.f))
         return fail(IABN_ERR_PARAM, "momentum must lie in [0, 1]");
     if ((rc = check_workspace(N, C, HW, workspace, workspace_bytes))) return rc;
-    const bool vec = use_vector(HW, dtype, x, fm == kFwdInPlace ? nullptr : out);
+    const int vec = access_vec(HW, dtype, x, fm == kFwdInPlace ? nullptr : out, nullptr);
     const Geom g = make_geom(N, C, HW, dtype, vec);
     const FwdParams prm = {gamma,    beta, running_mean, running_var, save_mean, save_var,
                            fm == kFwdInPlace ? nullptr : out, eps, momentum, slope};
     const hipStream_t st = static_cast<hipStream_t>(stream);
     FusedPlan fp;
-    if (plan_fused(C, g, vec, false, &fp)) {
+    if (plan_fused(C, g, elem_bytes(dtype), false, fm == kFwdInPlace, &fp)) {
         if (!launch_fwd_fused(dtype, fm, x, g, fp, prm, st))
             return fail(IABN_ERR_HIP, "no %s kernel built for T=%d R=%d", fwd_name(fm), fp.T, fp.R);
         return launched(fwd_name(fm));
@@ -207,12 +213,12 @@ int backward_impl(int bm, bool ii, const void* u, const void* zs, void* dz_dx, i
         return fail(IABN_ERR_NULL, "a tensor or parameter pointer is NULL");
     if ((rc = check_params(eps, slope))) return rc;
     if ((rc = check_workspace(N, C, HW, workspace, workspace_bytes))) return rc;
-    const bool vec = vector_ok(HW, dtype, u, dz_dx, bm == kBwdFromXZ ? zs : nullptr);
+    const int vec = access_vec(HW, dtype, u, dz_dx, bm == kBwdFromXZ ? zs : nullptr);
     const Geom g = make_geom(N, C, HW, dtype, vec);
     const BwdParams prm = {gamma, beta, save_mean, save_var, dgamma, dbeta, eps, slope, ii ? 1 : 0};
     const hipStream_t st = static_cast<hipStream_t>(stream);
     FusedPlan fp;
-    if (plan_fused(C, g, vec, true, &fp)) {
+    if (plan_fused(C, g, elem_bytes(dtype), true, bm == kBwdFromZ, &fp)) {
         if (!launch_bwd_fused(dtype, bm, u, zs, dz_dx, g, fp, prm, st))
             return fail(IABN_ERR_HIP, "no %s kernel built for T=%d R=%d", bwd_name(bm, ii), fp.T, fp.R);
         return launched(bwd_name(bm, ii));
@@ -264,7 +270,7 @@ int iabn_forward_stats(const void* x, int dtype, int64_t N, int64_t C, int64_t H
     if (empty(N, C, HW)) return ok();
     if (x == nullptr) return fail(IABN_ERR_NULL, "x is NULL");
     if ((rc = check_workspace(N, C, HW, workspace, workspace_bytes))) return rc;
-    const bool vec = use_vector(HW, dtype, x, nullptr);
+    const int vec = access_vec(HW, dtype, x, nullptr, nullptr);
     const Geom g = make_geom(N, C, HW, dtype, vec);
     launch_fwd_stats(dtype, vec, x, g, static_cast<Partial*>(workspace),
                              static_cast<hipStream_t>(stream));
@@ -285,7 +291,7 @@ int iabn_forward_apply(void* x_z, int dtype, const float* gamma, const float* be
     if (!(momentum >= 0.f && momentum <= 1.f))
         return fail(IABN_ERR_PARAM, "momentum must lie in [0, 1]");
     if ((rc = check_workspace(N, C, HW, workspace, workspace_bytes))) return rc;
-    const bool vec = use_vector(HW, dtype, x_z, nullptr);
+    const int vec = access_vec(HW, dtype, x_z, nullptr, nullptr);
     const Geom g = make_geom(N, C, HW, dtype, vec);
     const FwdParams prm = {gamma, beta, running_mean, running_var, save_mean, save_var,
                            nullptr, eps, momentum, slope};
@@ -313,7 +319,7 @@ int iabn_forward_eval(void* x_z, int dtype, const float* gamma, const float* bet
     if (!x_z || !gamma || !beta || !running_mean || !running_var)
         return fail(IABN_ERR_NULL, "a tensor or parameter pointer is NULL");
     if ((rc = check_params(eps, slope))) return rc;
-    const bool vec = use_vector(HW, dtype, x_z, nullptr);
+    const int vec = access_vec(HW, dtype, x_z, nullptr, nullptr);
     const Geom g = make_geom(N, C, HW, dtype, vec);
     const FwdParams prm = {gamma, beta, const_cast<float*>(running_mean),
                            const_cast<float*>(running_var), nullptr, nullptr, nullptr, eps, 0.f,
@@ -334,7 +340,7 @@ int iabn_backward_reduce(const void* z, const void* dz, int dtype, const float* 
     if (!(slope > 0.f) || !std::isfinite(slope))
         return fail(IABN_ERR_PARAM, "slope must be finite and > 0 (the activation must be invertible)");
     if ((rc = check_workspace(N, C, HW, workspace, workspace_bytes))) return rc;
-    const bool vec = use_vector(HW, dtype, z, dz);
+    const int vec = access_vec(HW, dtype, z, dz, nullptr);
     const Geom g = make_geom(N, C, HW, dtype, vec);
     const BwdParams prm = {gamma, beta, nullptr, nullptr, nullptr, nullptr, 1.f, slope, 0};
     launch_bwd_reduce(dtype, vec, z, static_cast<const void*>(nullptr), dz, g, prm,
@@ -354,7 +360,7 @@ int iabn_backward_apply(const void* z, void* dz_dx, int dtype, const float* gamm
         return fail(IABN_ERR_NULL, "a tensor or parameter pointer is NULL");
     if ((rc = check_params(eps, slope))) return rc;
     if ((rc = check_workspace(N, C, HW, workspace, workspace_bytes))) return rc;
-    const bool vec = use_vector(HW, dtype, z, dz_dx);
+    const int vec = access_vec(HW, dtype, z, dz_dx, nullptr);
     const Geom g = make_geom(N, C, HW, dtype, vec);
     const BwdParams prm = {gamma, beta, nullptr, save_var, dgamma, dbeta, eps, slope, 0};
     launch_bwd_apply(dtype, vec, z, static_cast<const void*>(nullptr), dz_dx, g,
@@ -418,7 +424,7 @@ int iabn_ckpt_recompute(const void* xhat, void* z, int dtype, const float* gamma
     if (!xhat || !z || !gamma || !beta)
         return fail(IABN_ERR_NULL, "a tensor or parameter pointer is NULL");
     if ((rc = check_params(1.f, slope))) return rc;
-    const bool vec = use_vector(HW, dtype, xhat, z);
+    const int vec = access_vec(HW, dtype, xhat, z, nullptr);
     const Geom g = make_geom(N, C, HW, dtype, vec);
     launch_recompute(dtype, vec, xhat, z, g, gamma, beta, slope,
                               static_cast<hipStream_t>(stream));

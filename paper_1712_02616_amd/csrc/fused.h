@@ -4,6 +4,8 @@
 // register budget.
 #pragma once
 
+#include <type_traits>
+
 #include "common.h"
 
 namespace iabn_impl {
@@ -17,12 +19,29 @@ namespace iabn_impl {
 // of its channel, so a wave touches consecutive 16-byte vectors.  The only
 // synchronisation is the block barrier around the channel's reduction.
 
-typedef uint32_t raw16_t __attribute__((ext_vector_type(4)));
+// One access of VEC elements of storage type DT, kept raw (undecoded) in
+// registers: 16 bytes as 4 dwords, 8 bytes as one 64-bit value (a 2-dword
+// vector made the compiler shuffle registers through AGPRs), 4 bytes as one
+// dword, and a 2-byte element in the low half of a dword.
+template <int DT, int VEC>
+struct RawAccess {
+    using T = typename Elem<DT>::T;
+    static constexpr int kBytes = VEC * static_cast<int>(sizeof(T));
+    typedef uint32_t v4 __attribute__((ext_vector_type(4)));
+    // What is held in registers.
+    using reg = typename std::conditional<
+        kBytes == 16, v4, typename std::conditional<kBytes == 8, uint64_t, uint32_t>::type>::type;
+    // What is read from and written to memory.
+    using mem = typename std::conditional<kBytes == 2, uint16_t, reg>::type;
+};
+
+template <int DT, int VEC>
+using raw_t = typename RawAccess<DT, VEC>::reg;
 
 // Hide a value from the optimiser (an empty asm that "may change" it).  Used
 // after the reduction barrier so that the apply phase keeps only the raw
-// 16-byte registers alive and converts them again, instead of keeping the
-// twice-as-large fp32 values (and 64-bit addresses) from the first phase.
+// registers alive and converts them again, instead of keeping the larger
+// fp32 values (and 64-bit addresses) from the first phase.
 template <typename V>
 __device__ __forceinline__ void opaque(V& v) {
     asm volatile("" : "+v"(v));
@@ -33,20 +52,26 @@ __device__ __forceinline__ void opaque(V& v) {
 // are already all in flight), and past the block's register budget it spills.
 __device__ __forceinline__ void sched_fence() { __builtin_amdgcn_sched_barrier(0); }
 
-template <int HINT>
-__device__ __forceinline__ raw16_t load_raw(const void* __restrict__ base, uint64_t idx) {
-    const raw16_t* p = static_cast<const raw16_t*>(base) + idx;
-    return HINT == kStream ? __builtin_nontemporal_load(p) : *p;
+template <int DT, int VEC, int HINT>
+__device__ __forceinline__ raw_t<DT, VEC> load_raw(const void* __restrict__ base, uint64_t idx) {
+    using mem = typename RawAccess<DT, VEC>::mem;
+    const mem* p = static_cast<const mem*>(base) + idx;
+    return static_cast<raw_t<DT, VEC>>(HINT == kStream ? __builtin_nontemporal_load(p) : *p);
 }
 
 template <int DT, int VEC>
-__device__ __forceinline__ void unpack(raw16_t r, float (&v)[VEC]) {
+__device__ __forceinline__ void unpack(raw_t<DT, VEC> r, float (&v)[VEC]) {
     using T = typename Elem<DT>::T;
-    typedef T vt __attribute__((ext_vector_type(VEC)));
-    typedef float vf __attribute__((ext_vector_type(VEC)));
-    const vf f = __builtin_convertvector(__builtin_bit_cast(vt, r), vf);
+    if constexpr (VEC == 1) {
+        v[0] = static_cast<float>(
+            __builtin_bit_cast(T, static_cast<typename RawAccess<DT, VEC>::mem>(r)));
+    } else {
+        typedef T vt __attribute__((ext_vector_type(VEC)));
+        typedef float vf __attribute__((ext_vector_type(VEC)));
+        const vf f = __builtin_convertvector(__builtin_bit_cast(vt, r), vf);
 #pragma unroll
-    for (int k = 0; k < VEC; ++k) v[k] = f[k];
+        for (int k = 0; k < VEC; ++k) v[k] = f[k];
+    }
 }
 
 // Per-wave (shift, s1, s2, n) of a block, combined by wave 0 in a fixed

@@ -38,7 +38,7 @@ __device__ __forceinline__ void bwd_fused_channel(const void* __restrict__ u,
     // fwd_fused_channel).  kBwdFromXZ first loads z (into the registers x
     // will use) and dz, turns z into sign bits, and only then loads x, so
     // that no more than two tensors' worth of registers is live.
-    raw16_t ku[R], kg[R];
+    raw_t<DT, VEC> ku[R], kg[R];
     uint32_t negm[NW];
 #pragma unroll
     for (int q = 0; q < NW; ++q) negm[q] = 0u;
@@ -62,8 +62,8 @@ __device__ __forceinline__ void bwd_fused_channel(const void* __restrict__ u,
             bool live;
             const uint64_t i1 = resident_index(k, sz, live);
             if (live) {
-                ku[k] = load_raw<kStream>(zs, i1);
-                kg[k] = load_raw<kStream>(dzdx, i1);
+                ku[k] = load_raw<DT, VEC, kStream>(zs, i1);
+                kg[k] = load_raw<DT, VEC, kStream>(dzdx, i1);
             }
         }
 #pragma unroll
@@ -85,7 +85,7 @@ __device__ __forceinline__ void bwd_fused_channel(const void* __restrict__ u,
         for (int k = 0; k < R; ++k) {
             bool live;
             const uint64_t i1 = resident_index(k, sp, live);
-            if (live) ku[k] = load_raw<kStream>(u, i1);
+            if (live) ku[k] = load_raw<DT, VEC, kStream>(u, i1);
         }
     } else {
 #pragma unroll
@@ -93,8 +93,8 @@ __device__ __forceinline__ void bwd_fused_channel(const void* __restrict__ u,
             bool live;
             const uint64_t i1 = resident_index(k, sp, live);
             if (live) {
-                ku[k] = load_raw<kStream>(u, i1);
-                kg[k] = load_raw<kStream>(dzdx, i1);
+                ku[k] = load_raw<DT, VEC, kStream>(u, i1);
+                kg[k] = load_raw<DT, VEC, kStream>(dzdx, i1);
             }
         }
     }
@@ -128,12 +128,12 @@ __device__ __forceinline__ void bwd_fused_channel(const void* __restrict__ u,
     }
     auto accumulate = [&](uint64_t i1) {
         float tu[VEC], tz[VEC], tg[VEC];
-        unpack<DT, VEC>(load_raw<kCached>(u, i1), tu);
-        if constexpr (XZ) unpack<DT, VEC>(load_raw<kCached>(zs, i1), tz);
+        unpack<DT, VEC>(load_raw<DT, VEC, kCached>(u, i1), tu);
+        if constexpr (XZ) unpack<DT, VEC>(load_raw<DT, VEC, kCached>(zs, i1), tz);
         else
 #pragma unroll
             for (int e = 0; e < VEC; ++e) tz[e] = 0.f;
-        unpack<DT, VEC>(load_raw<kCached>(dzdx, i1), tg);
+        unpack<DT, VEC>(load_raw<DT, VEC, kCached>(dzdx, i1), tg);
         float sdy = 0.f, sdyw = 0.f;
 #pragma unroll
         for (int e = 0; e < VEC; ++e) {
@@ -174,7 +174,7 @@ __device__ __forceinline__ void bwd_fused_channel(const void* __restrict__ u,
         prm.dgamma[c] = static_cast<float>(sdyw);
         prm.dbeta[c] = static_cast<float>(dbeta);
     }
-    auto emit = [&](raw16_t ru, raw16_t rz, raw16_t rg, uint64_t idx) {
+    auto emit = [&](raw_t<DT, VEC> ru, raw_t<DT, VEC> rz, raw_t<DT, VEC> rg, uint64_t idx) {
         float tu[VEC], tz[VEC], tg[VEC];
         unpack<DT, VEC>(ru, tu);
         if constexpr (XZ) unpack<DT, VEC>(rz, tz);
@@ -217,21 +217,21 @@ __device__ __forceinline__ void bwd_fused_channel(const void* __restrict__ u,
         }
         sched_fence();
     }
-    const raw16_t zero16 = {0u, 0u, 0u, 0u};
+    const raw_t<DT, VEC> zero16 = {};
     if constexpr (STRIP) {
 #pragma unroll 1
         for (uint32_t k = R; k < nstrips; ++k) {
             const uint64_t i1 = sq.off + tid2;
-            emit(load_raw<kStream>(u, i1), XZ ? load_raw<kStream>(zs, i1) : zero16,
-                 load_raw<kStream>(dzdx, i1), i1);
+            emit(load_raw<DT, VEC, kStream>(u, i1), XZ ? load_raw<DT, VEC, kStream>(zs, i1) : zero16,
+                 load_raw<DT, VEC, kStream>(dzdx, i1), i1);
             strip_next<T>(g, sq);
         }
     } else {
 #pragma unroll 1
         for (uint32_t v = tid2 + R * T; v < g.vchan; v += T) {
             const uint64_t i1 = access_index(g, cbase, v);
-            emit(load_raw<kStream>(u, i1), XZ ? load_raw<kStream>(zs, i1) : zero16,
-                 load_raw<kStream>(dzdx, i1), i1);
+            emit(load_raw<DT, VEC, kStream>(u, i1), XZ ? load_raw<DT, VEC, kStream>(zs, i1) : zero16,
+                 load_raw<DT, VEC, kStream>(dzdx, i1), i1);
         }
     }
 }
@@ -245,46 +245,73 @@ __global__ __launch_bounds__(T) void bwd_fused_kernel(const void* __restrict__ u
     bwd_fused_channel<DT, VEC, T, R, STRIP, BM>(u, zs, dzdx, g, prm, blockIdx.x);
 }
 
-#define IABN_FUSED_CASE(KERNEL, MODE, TT, RR, ...)                                             \
+#define IABN_FUSED_CASE(TT, RR)                                                              \
     if (fp.T == TT && fp.R == RR) {                                                           \
         if (kUseStrips && g.vrow % TT == 0 && g.vchan / TT >= RR)                             \
-            KERNEL<DT, V, TT, RR, true, MODE><<<grid, TT, lds, st>>>(__VA_ARGS__);            \
+            bwd_fused_kernel<DT, V, TT, RR, true, BM><<<grid, TT, lds, st>>>(u, zs, dzdx, g, prm);  \
         else                                                                                  \
-            KERNEL<DT, V, TT, RR, false, MODE><<<grid, TT, lds, st>>>(__VA_ARGS__);           \
+            bwd_fused_kernel<DT, V, TT, RR, false, BM><<<grid, TT, lds, st>>>(u, zs, dzdx, g, prm); \
+        return true;                                                                          \
+    }
+// Narrower accesses: the general mapping only (see fused_fwd.hip).
+#define IABN_FUSED_CASE_GENERAL(TT, RR)                                                      \
+    if (fp.T == TT && fp.R == RR) {                                                           \
+        bwd_fused_kernel<DT, V, TT, RR, false, BM><<<grid, TT, lds, st>>>(u, zs, dzdx, g, prm);     \
         return true;                                                                          \
     }
 
-template <int DT, int BM>
-bool launch_bwd_fused(const void* u, const void* zs, void* dzdx, const Geom& g,
-                      const FusedPlan& fp, const BwdParams& prm, hipStream_t st) {
-    constexpr int V = 16 / sizeof(typename Elem<DT>::T);
+template <int DT, int V, int BM>
+bool launch_v(const void* u, const void* zs, void* dzdx, const Geom& g, const FusedPlan& fp,
+              const BwdParams& prm, hipStream_t st) {
     const dim3 grid = fused_grid(g, fp);
     const size_t lds = fused_lds(kFusedBwdBlocksPerCU);
-    IABN_FUSED_CASE(bwd_fused_kernel, BM, 256, 4, u, zs, dzdx, g, prm)
-    IABN_FUSED_CASE(bwd_fused_kernel, BM, 512, 4, u, zs, dzdx, g, prm)
-    IABN_FUSED_CASE(bwd_fused_kernel, BM, 256, 16, u, zs, dzdx, g, prm)
-    IABN_FUSED_CASE(bwd_fused_kernel, BM, 512, 16, u, zs, dzdx, g, prm)
-    IABN_FUSED_CASE(bwd_fused_kernel, BM, 1024, 11, u, zs, dzdx, g, prm)
+    if constexpr (V * sizeof(typename Elem<DT>::T) == 16) {
+        IABN_FUSED_CASE(256, 4)
+        IABN_FUSED_CASE(512, 4)
+        IABN_FUSED_CASE(256, 16)
+        IABN_FUSED_CASE(512, 16)
+        IABN_FUSED_CASE(1024, 11)
+    } else if constexpr (BM == kBwdFromZ) {
+        IABN_FUSED_CASE_GENERAL(256, 4)
+        IABN_FUSED_CASE_GENERAL(256, 8)
+        IABN_FUSED_CASE_GENERAL(256, 16)
+        IABN_FUSED_CASE_GENERAL(512, 16)
+        IABN_FUSED_CASE_GENERAL(1024, 16)
+    }
     return false;
 }
 
 #undef IABN_FUSED_CASE
+#undef IABN_FUSED_CASE_GENERAL
+
+template <int DT, int BM>
+bool launch_dt(int vec, const void* u, const void* zs, void* dzdx, const Geom& g,
+               const FusedPlan& fp, const BwdParams& prm, hipStream_t st) {
+    constexpr int W = 16 / static_cast<int>(sizeof(typename Elem<DT>::T));
+    if (vec == W) return launch_v<DT, W, BM>(u, zs, dzdx, g, fp, prm, st);
+    if (vec == W / 2) return launch_v<DT, W / 2, BM>(u, zs, dzdx, g, fp, prm, st);
+    if constexpr (W / 4 > 1) {
+        if (vec == W / 4) return launch_v<DT, W / 4, BM>(u, zs, dzdx, g, fp, prm, st);
+    }
+    if (vec == 1) return launch_v<DT, 1, BM>(u, zs, dzdx, g, fp, prm, st);
+    return false;
+}
 
 template <int BM>
-bool launch_dt(int dtype, const void* u, const void* zs, void* dzdx, const Geom& g,
+bool launch_bm(int dtype, const void* u, const void* zs, void* dzdx, const Geom& g,
                const FusedPlan& fp, const BwdParams& prm, hipStream_t st) {
-    return dtype == IABN_F32   ? launch_bwd_fused<IABN_F32, BM>(u, zs, dzdx, g, fp, prm, st)
-           : dtype == IABN_F16 ? launch_bwd_fused<IABN_F16, BM>(u, zs, dzdx, g, fp, prm, st)
-                               : launch_bwd_fused<IABN_BF16, BM>(u, zs, dzdx, g, fp, prm, st);
+    return dtype == IABN_F32   ? launch_dt<IABN_F32, BM>(g.vec, u, zs, dzdx, g, fp, prm, st)
+           : dtype == IABN_F16 ? launch_dt<IABN_F16, BM>(g.vec, u, zs, dzdx, g, fp, prm, st)
+                               : launch_dt<IABN_BF16, BM>(g.vec, u, zs, dzdx, g, fp, prm, st);
 }
 
 }  // namespace
 
 bool launch_bwd_fused(int dtype, int bm, const void* u, const void* zs, void* dzdx, const Geom& g,
                       const FusedPlan& fp, const BwdParams& prm, hipStream_t st) {
-    return bm == kBwdFromXZ     ? launch_dt<kBwdFromXZ>(dtype, u, zs, dzdx, g, fp, prm, st)
-           : bm == kBwdFromXhat ? launch_dt<kBwdFromXhat>(dtype, u, zs, dzdx, g, fp, prm, st)
-                                : launch_dt<kBwdFromZ>(dtype, u, zs, dzdx, g, fp, prm, st);
+    return bm == kBwdFromXZ     ? launch_bm<kBwdFromXZ>(dtype, u, zs, dzdx, g, fp, prm, st)
+           : bm == kBwdFromXhat ? launch_bm<kBwdFromXhat>(dtype, u, zs, dzdx, g, fp, prm, st)
+                                : launch_bm<kBwdFromZ>(dtype, u, zs, dzdx, g, fp, prm, st);
 }
 
 }  // namespace iabn_impl

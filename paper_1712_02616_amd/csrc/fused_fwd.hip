@@ -41,7 +41,7 @@ __device__ __forceinline__ void fwd_fused_emit(void* __restrict__ xz, uint64_t i
 // registers) and the remainder (loaded again).
 template <int DT, int VEC, int T, int R, bool STRIP, int FM, bool SMALL_SLOPE>
 __device__ __forceinline__ void fwd_fused_apply(void* __restrict__ xz, const Geom& g, uint32_t c,
-                                                uint32_t tid, const raw16_t (&keep)[R],
+                                                uint32_t tid, const raw_t<DT, VEC> (&keep)[R],
                                                 const FwdApplyK& kk) {
     const uint64_t cbase = static_cast<uint64_t>(c) * g.vrow;
     const uint32_t nstrips = STRIP ? g.vchan / T : 0;
@@ -71,7 +71,7 @@ __device__ __forceinline__ void fwd_fused_apply(void* __restrict__ xz, const Geo
         for (uint32_t k = R; k < nstrips; ++k) {
             const uint64_t idx = sq.off + tid;
             float t[VEC];
-            unpack<DT, VEC>(load_raw<kStream>(xz, idx), t);
+            unpack<DT, VEC>(load_raw<DT, VEC, kStream>(xz, idx), t);
             fwd_fused_emit<DT, VEC, FM, SMALL_SLOPE>(xz, idx, t, kk);
             strip_next<T>(g, sq);
         }
@@ -80,7 +80,7 @@ __device__ __forceinline__ void fwd_fused_apply(void* __restrict__ xz, const Geo
         for (uint32_t v = tid + R * T; v < g.vchan; v += T) {
             const uint64_t idx = access_index(g, cbase, v);
             float t[VEC];
-            unpack<DT, VEC>(load_raw<kStream>(xz, idx), t);
+            unpack<DT, VEC>(load_raw<DT, VEC, kStream>(xz, idx), t);
             fwd_fused_emit<DT, VEC, FM, SMALL_SLOPE>(xz, idx, t, kk);
         }
     }
@@ -95,7 +95,6 @@ __device__ __forceinline__ void fwd_fused_channel(void* __restrict__ xz, const G
     const uint64_t cbase = static_cast<uint64_t>(c) * g.vrow;
     const uint32_t tid = threadIdx.x;
     const uint32_t nstrips = STRIP ? g.vchan / T : 0;
-    raw16_t* const xv = static_cast<raw16_t*>(xz);
     // Per-channel inputs before the data loads (see bwd_fused_channel).
     const float gamma_c = prm.gamma[c], beta_c = prm.beta[c];
     float rm_c = 0.f, rv_c = 0.f;
@@ -109,16 +108,16 @@ __device__ __forceinline__ void fwd_fused_channel(void* __restrict__ xz, const G
     // again by the apply and go through the caches.  (Measured: non-temporal
     // register-resident loads cut the forward over the backbone sweep by 12%
     // and the backward by 7%.)
-    raw16_t keep[R];
+    raw_t<DT, VEC> keep[R];
     StripPos sp = strip_begin(g, c);
 #pragma unroll
     for (int k = 0; k < R; ++k) {
         if constexpr (STRIP) {
-            keep[k] = load_raw<kStream>(xv, sp.off + tid);
+            keep[k] = load_raw<DT, VEC, kStream>(xz, sp.off + tid);
             strip_next<T>(g, sp);
         } else {
             const uint32_t v = tid + k * T;
-            if (v < g.vchan) keep[k] = load_raw<kStream>(xz, access_index(g, cbase, v));
+            if (v < g.vchan) keep[k] = load_raw<DT, VEC, kStream>(xz, access_index(g, cbase, v));
         }
     }
     float shift = 0.f, s1 = 0.f, s2 = 0.f;
@@ -128,7 +127,7 @@ __device__ __forceinline__ void fwd_fused_channel(void* __restrict__ xz, const G
         unpack<DT, VEC>(keep[0], t);
         shift = t[0];
     }
-    auto accumulate = [&](raw16_t r) {
+    auto accumulate = [&](raw_t<DT, VEC> r) {
         float t[VEC];
         unpack<DT, VEC>(r, t);
 #pragma unroll
@@ -157,13 +156,13 @@ __device__ __forceinline__ void fwd_fused_channel(void* __restrict__ xz, const G
     if constexpr (STRIP) {
 #pragma unroll 1
         for (uint32_t k = R; k < nstrips; ++k) {
-            accumulate((xv + sp.off)[tid]);
+            accumulate(load_raw<DT, VEC, kCached>(xz, sp.off + tid));
             strip_next<T>(g, sp);
         }
     } else {
 #pragma unroll 1
         for (uint32_t v = tid + R * T; v < g.vchan; v += T)
-            accumulate(load_raw<kCached>(xz, access_index(g, cbase, v)));
+            accumulate(load_raw<DT, VEC, kCached>(xz, access_index(g, cbase, v)));
     }
 
     double mean, var;
@@ -217,46 +216,75 @@ __global__ __launch_bounds__(T) void fwd_fused_kernel(void* __restrict__ xz, Geo
     fwd_fused_channel<DT, VEC, T, R, STRIP, FM>(xz, g, prm, blockIdx.x);
 }
 
-#define IABN_FUSED_CASE(KERNEL, MODE, TT, RR, ...)                                             \
+#define IABN_FUSED_CASE(TT, RR)                                                              \
     if (fp.T == TT && fp.R == RR) {                                                           \
         if (kUseStrips && g.vrow % TT == 0 && g.vchan / TT >= RR)                             \
-            KERNEL<DT, V, TT, RR, true, MODE><<<grid, TT, lds, st>>>(__VA_ARGS__);            \
+            fwd_fused_kernel<DT, V, TT, RR, true, FM><<<grid, TT, lds, st>>>(xz, g, prm);     \
         else                                                                                  \
-            KERNEL<DT, V, TT, RR, false, MODE><<<grid, TT, lds, st>>>(__VA_ARGS__);           \
+            fwd_fused_kernel<DT, V, TT, RR, false, FM><<<grid, TT, lds, st>>>(xz, g, prm);    \
+        return true;                                                                          \
+    }
+// Narrower accesses: rows of odd length rarely hold whole strips, so only
+// the general mapping is built.
+#define IABN_FUSED_CASE_GENERAL(TT, RR)                                                      \
+    if (fp.T == TT && fp.R == RR) {                                                           \
+        fwd_fused_kernel<DT, V, TT, RR, false, FM><<<grid, TT, lds, st>>>(xz, g, prm);        \
         return true;                                                                          \
     }
 
-template <int DT, int FM>
-bool launch_fwd_fused(void* xz, const Geom& g, const FusedPlan& fp, const FwdParams& prm,
-                      hipStream_t st) {
-    constexpr int V = 16 / sizeof(typename Elem<DT>::T);
+template <int DT, int V, int FM>
+bool launch_v(void* xz, const Geom& g, const FusedPlan& fp, const FwdParams& prm, hipStream_t st) {
     const dim3 grid = fused_grid(g, fp);
     const size_t lds = fused_lds(kFusedFwdBlocksPerCU);
-    IABN_FUSED_CASE(fwd_fused_kernel, FM, 256, 4, xz, g, prm)
-    IABN_FUSED_CASE(fwd_fused_kernel, FM, 512, 4, xz, g, prm)
-    IABN_FUSED_CASE(fwd_fused_kernel, FM, 256, 16, xz, g, prm)
-    IABN_FUSED_CASE(fwd_fused_kernel, FM, 512, 16, xz, g, prm)
-    IABN_FUSED_CASE(fwd_fused_kernel, FM, 1024, 16, xz, g, prm)
+    if constexpr (V * sizeof(typename Elem<DT>::T) == 16) {
+        IABN_FUSED_CASE(256, 4)
+        IABN_FUSED_CASE(512, 4)
+        IABN_FUSED_CASE(256, 16)
+        IABN_FUSED_CASE(512, 16)
+        IABN_FUSED_CASE(1024, 16)
+    } else if constexpr (FM == kFwdInPlace) {
+        IABN_FUSED_CASE_GENERAL(256, 4)
+        IABN_FUSED_CASE_GENERAL(256, 8)
+        IABN_FUSED_CASE_GENERAL(256, 16)
+        IABN_FUSED_CASE_GENERAL(512, 16)
+        IABN_FUSED_CASE_GENERAL(1024, 16)
+    }
     return false;
 }
 
 #undef IABN_FUSED_CASE
+#undef IABN_FUSED_CASE_GENERAL
+
+// Elements per access: 16 bytes, or the narrower widths of rows that are not
+// a multiple of 16 bytes.
+template <int DT, int FM>
+bool launch_dt(int vec, void* xz, const Geom& g, const FusedPlan& fp, const FwdParams& prm,
+               hipStream_t st) {
+    constexpr int W = 16 / static_cast<int>(sizeof(typename Elem<DT>::T));
+    if (vec == W) return launch_v<DT, W, FM>(xz, g, fp, prm, st);
+    if (vec == W / 2) return launch_v<DT, W / 2, FM>(xz, g, fp, prm, st);
+    if constexpr (W / 4 > 1) {
+        if (vec == W / 4) return launch_v<DT, W / 4, FM>(xz, g, fp, prm, st);
+    }
+    if (vec == 1) return launch_v<DT, 1, FM>(xz, g, fp, prm, st);
+    return false;
+}
 
 template <int FM>
-bool launch_dt(int dtype, void* xz, const Geom& g, const FusedPlan& fp, const FwdParams& prm,
+bool launch_fm(int dtype, void* xz, const Geom& g, const FusedPlan& fp, const FwdParams& prm,
                hipStream_t st) {
-    return dtype == IABN_F32   ? launch_fwd_fused<IABN_F32, FM>(xz, g, fp, prm, st)
-           : dtype == IABN_F16 ? launch_fwd_fused<IABN_F16, FM>(xz, g, fp, prm, st)
-                               : launch_fwd_fused<IABN_BF16, FM>(xz, g, fp, prm, st);
+    return dtype == IABN_F32   ? launch_dt<IABN_F32, FM>(g.vec, xz, g, fp, prm, st)
+           : dtype == IABN_F16 ? launch_dt<IABN_F16, FM>(g.vec, xz, g, fp, prm, st)
+                               : launch_dt<IABN_BF16, FM>(g.vec, xz, g, fp, prm, st);
 }
 
 }  // namespace
 
 bool launch_fwd_fused(int dtype, int fm, void* xz, const Geom& g, const FusedPlan& fp,
                       const FwdParams& prm, hipStream_t st) {
-    return fm == kFwdOut    ? launch_dt<kFwdOut>(dtype, xz, g, fp, prm, st)
-           : fm == kFwdCkpt ? launch_dt<kFwdCkpt>(dtype, xz, g, fp, prm, st)
-                            : launch_dt<kFwdInPlace>(dtype, xz, g, fp, prm, st);
+    return fm == kFwdOut    ? launch_fm<kFwdOut>(dtype, xz, g, fp, prm, st)
+           : fm == kFwdCkpt ? launch_fm<kFwdCkpt>(dtype, xz, g, fp, prm, st)
+                            : launch_fm<kFwdInPlace>(dtype, xz, g, fp, prm, st);
 }
 
 }  // namespace iabn_impl

@@ -12,17 +12,18 @@ namespace iabn_impl {
 
 // ---- streaming kernels (stream.hip)
 
-void launch_fwd_stats(int dtype, bool vec, const void* x, const Geom& g, Partial* part,
+// vec: elements per access (Geom::vec).
+void launch_fwd_stats(int dtype, int vec, const void* x, const Geom& g, Partial* part,
                       hipStream_t st);
 // train = false is inference (in place); otherwise fm is the output mode.
-void launch_fwd_apply(int dtype, bool vec, void* xz, const Geom& g, const Partial* part,
+void launch_fwd_apply(int dtype, int vec, void* xz, const Geom& g, const Partial* part,
                       const FwdParams& prm, bool train, int fm, hipStream_t st);
-void launch_bwd_reduce(int dtype, bool vec, const void* u, const void* zs, const void* dz,
+void launch_bwd_reduce(int dtype, int vec, const void* u, const void* zs, const void* dz,
                        const Geom& g, const BwdParams& prm, int bm, Partial* part, hipStream_t st);
-void launch_bwd_apply(int dtype, bool vec, const void* u, const void* zs, void* dzdx,
+void launch_bwd_apply(int dtype, int vec, const void* u, const void* zs, void* dzdx,
                       const Geom& g, const Partial* part, const BwdParams& prm, int bm,
                       hipStream_t st);
-void launch_recompute(int dtype, bool vec, const void* xhat, void* z, const Geom& g,
+void launch_recompute(int dtype, int vec, const void* xhat, void* z, const Geom& g,
                       const float* gamma, const float* beta, float slope, hipStream_t st);
 
 // ---- channel-resident kernels (fused_fwd.hip, fused_bwd.hip)
@@ -64,12 +65,26 @@ constexpr bool kUseStrips = true;
 constexpr FusedPlan kFwdLadder[] = {{256, 4}, {512, 4}, {256, 16}, {512, 16}, {1024, 16}};
 constexpr FusedPlan kBwdLadder[] = {{256, 4}, {512, 4}, {256, 16}, {512, 16}, {1024, 11}};
 
-inline bool plan_fused(int64_t C, const Geom& g, bool vector, bool backward, FusedPlan* out) {
-    if (!vector || C < kFusedMinChannels) return false;
+// Accesses narrower than 16 bytes (rows whose length is not a multiple of
+// 16 bytes: 14x14 or 7x7 maps in fp16, for instance) hold the same
+// elements in more, smaller registers; one ladder serves both directions.
+// Built for InPlace-ABN's own forward and backward only (the comparison
+// blocks take the streaming kernels on such shapes).  (One wave per channel
+// for the small channels of 7x7 maps measured no faster than these rungs.)
+constexpr FusedPlan kNarrowLadder[] = {{256, 4}, {256, 8}, {256, 16}, {512, 16}, {1024, 16}};
+
+// elem_bytes: storage size; narrow_ok: whether this entry point has narrow
+// channel-resident kernels.
+inline bool plan_fused(int64_t C, const Geom& g, int elem_bytes, bool backward, bool narrow_ok,
+                       FusedPlan* out) {
+    if (C < kFusedMinChannels) return false;
+    const bool wide = static_cast<int>(g.vec) * elem_bytes == 16;
+    if (!wide && !narrow_ok) return false;
+    const FusedPlan* ladder = !wide ? kNarrowLadder : backward ? kBwdLadder : kFwdLadder;
+    const int n = !wide      ? int(sizeof kNarrowLadder / sizeof kNarrowLadder[0])
+                  : backward ? int(sizeof kBwdLadder / sizeof kBwdLadder[0])
+                             : int(sizeof kFwdLadder / sizeof kFwdLadder[0]);
     const int64_t A = g.vchan;
-    const FusedPlan* ladder = backward ? kBwdLadder : kFwdLadder;
-    const int n = backward ? int(sizeof kBwdLadder / sizeof kBwdLadder[0])
-                           : int(sizeof kFwdLadder / sizeof kFwdLadder[0]);
     for (int i = 0; i < n; ++i) {
         if (A <= static_cast<int64_t>(ladder[i].T) * ladder[i].R || i == n - 1) {
             *out = ladder[i];

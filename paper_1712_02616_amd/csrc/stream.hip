@@ -382,36 +382,43 @@ __global__ __launch_bounds__(kThreads) void bwd_apply_kernel(const void* __restr
 
 dim3 grid_of(const Geom& g) { return dim3(g.C * g.P); }
 
-// Dispatch on dtype and access width.
-template <template <int, int> class Launch, typename... A>
-void dispatch(int dtype, bool vector, A&&... args) {
-    switch (dtype) {
-        case IABN_F32:
-            if (vector) Launch<IABN_F32, 4>::run(args...);
-            else Launch<IABN_F32, 1>::run(args...);
-            break;
-        case IABN_F16:
-            if (vector) Launch<IABN_F16, 8>::run(args...);
-            else Launch<IABN_F16, 1>::run(args...);
-            break;
-        default:
-            if (vector) Launch<IABN_BF16, 8>::run(args...);
-            else Launch<IABN_BF16, 1>::run(args...);
-            break;
+// Dispatch on dtype and access width (elements per access: 16, 8, 4 or 2
+// bytes' worth).
+template <template <int, int> class Launch, int DT, typename... A>
+void dispatch_vec(int vec, A&&... args) {
+    constexpr int W = 16 / static_cast<int>(sizeof(typename Elem<DT>::T));
+    if (vec == W) {
+        Launch<DT, W>::run(args...);
+    } else if (vec == W / 2) {
+        Launch<DT, W / 2>::run(args...);
+    } else if (W / 4 > 1 && vec == W / 4) {
+        Launch<DT, (W / 4 > 1 ? W / 4 : 1)>::run(args...);
+    } else {
+        Launch<DT, 1>::run(args...);
     }
 }
 
-// Accesses in flight per thread and batch: 2 x 16 bytes on the vector path
-// (measured best on the backbone sweep), 8 single elements on the scalar path.
-template <int VEC>
+template <template <int, int> class Launch, typename... A>
+void dispatch(int dtype, int vec, A&&... args) {
+    switch (dtype) {
+        case IABN_F32: dispatch_vec<Launch, IABN_F32>(vec, args...); break;
+        case IABN_F16: dispatch_vec<Launch, IABN_F16>(vec, args...); break;
+        default: dispatch_vec<Launch, IABN_BF16>(vec, args...); break;
+    }
+}
+
+// Accesses in flight per thread and batch: 32 bytes' worth (2 x 16 bytes on
+// the 16-byte path, measured best on the backbone sweep), at least 8.
+template <int DT, int VEC>
 constexpr int unroll() {
-    return VEC == 1 ? 8 : 2;
+    constexpr int bytes = VEC * static_cast<int>(sizeof(typename Elem<DT>::T));
+    return bytes >= 16 ? 2 : (32 / bytes < 8 ? 8 : 32 / bytes);
 }
 
 template <int DT, int VEC>
 struct LaunchFwdStats {
     static void run(const void* x, const Geom& g, Partial* part, hipStream_t st) {
-        fwd_stats_kernel<DT, VEC, unroll<VEC>()><<<grid_of(g), kThreads, 0, st>>>(x, g, part);
+        fwd_stats_kernel<DT, VEC, unroll<DT, VEC>()><<<grid_of(g), kThreads, 0, st>>>(x, g, part);
     }
 };
 
@@ -420,7 +427,7 @@ template <int DT, int VEC>
 struct LaunchFwdApply {
     static void run(void* xz, const Geom& g, const Partial* part, const FwdParams& prm, bool train,
                     int fm, hipStream_t st) {
-        constexpr int U = unroll<VEC>();
+        constexpr int U = unroll<DT, VEC>();
         const dim3 grid = grid_of(g);
         if (!train)
             fwd_apply_kernel<DT, VEC, U, false, kFwdInPlace><<<grid, kThreads, 0, st>>>(xz, g, part, prm);
@@ -437,7 +444,7 @@ template <int DT, int VEC>
 struct LaunchBwdReduce {
     static void run(const void* u, const void* zs, const void* dz, const Geom& g,
                     const BwdParams& prm, int bm, Partial* part, hipStream_t st) {
-        constexpr int U = unroll<VEC>();
+        constexpr int U = unroll<DT, VEC>();
         const dim3 grid = grid_of(g);
         if (bm == kBwdFromXZ)
             bwd_reduce_kernel<DT, VEC, U, kBwdFromXZ><<<grid, kThreads, 0, st>>>(u, zs, dz, g, prm, part);
@@ -452,7 +459,7 @@ template <int DT, int VEC>
 struct LaunchBwdApply {
     static void run(const void* u, const void* zs, void* dzdx, const Geom& g, const Partial* part,
                     const BwdParams& prm, int bm, hipStream_t st) {
-        constexpr int U = unroll<VEC>();
+        constexpr int U = unroll<DT, VEC>();
         const dim3 grid = grid_of(g);
         if (bm == kBwdFromXZ)
             bwd_apply_kernel<DT, VEC, U, kBwdFromXZ><<<grid, kThreads, 0, st>>>(u, zs, dzdx, g, part, prm);
@@ -473,28 +480,28 @@ struct LaunchRecompute {
 
 }  // namespace
 
-void launch_fwd_stats(int dtype, bool vec, const void* x, const Geom& g, Partial* part,
+void launch_fwd_stats(int dtype, int vec, const void* x, const Geom& g, Partial* part,
                       hipStream_t st) {
     dispatch<LaunchFwdStats>(dtype, vec, x, g, part, st);
 }
 
-void launch_fwd_apply(int dtype, bool vec, void* xz, const Geom& g, const Partial* part,
+void launch_fwd_apply(int dtype, int vec, void* xz, const Geom& g, const Partial* part,
                       const FwdParams& prm, bool train, int fm, hipStream_t st) {
     dispatch<LaunchFwdApply>(dtype, vec, xz, g, part, prm, train, fm, st);
 }
 
-void launch_bwd_reduce(int dtype, bool vec, const void* u, const void* zs, const void* dz,
+void launch_bwd_reduce(int dtype, int vec, const void* u, const void* zs, const void* dz,
                        const Geom& g, const BwdParams& prm, int bm, Partial* part, hipStream_t st) {
     dispatch<LaunchBwdReduce>(dtype, vec, u, zs, dz, g, prm, bm, part, st);
 }
 
-void launch_bwd_apply(int dtype, bool vec, const void* u, const void* zs, void* dzdx,
+void launch_bwd_apply(int dtype, int vec, const void* u, const void* zs, void* dzdx,
                       const Geom& g, const Partial* part, const BwdParams& prm, int bm,
                       hipStream_t st) {
     dispatch<LaunchBwdApply>(dtype, vec, u, zs, dzdx, g, part, prm, bm, st);
 }
 
-void launch_recompute(int dtype, bool vec, const void* xhat, void* z, const Geom& g,
+void launch_recompute(int dtype, int vec, const void* xhat, void* z, const Geom& g,
                       const float* gamma, const float* beta, float slope, hipStream_t st) {
     dispatch<LaunchRecompute>(dtype, vec, xhat, z, g, gamma, beta, slope, st);
 }

@@ -90,6 +90,17 @@ EDGE_CASES = [
     Case("manych_c1300_bf16", 4, 1300, 8192, "bf16", 29, dz_std=0.1),
     Case("manych_c520_f32", 4, 520, 4096, "f32", 30, dz_std=0.1),
     Case("manych_t256_c512_f16", 16, 512, 2048, "f16", 31, dz_std=0.1),
+    # Rows that are not a multiple of 16 bytes: the channel-resident kernels
+    # with 8-, 4- and 2-byte accesses (14x14 and 7x7 maps, and the like),
+    # including channels larger than the registers hold.
+    Case("narrow8_hw196_f16", 16, 512, 196, "f16", 32, dz_std=0.1, gamma_sign=True),
+    Case("narrow4_hw98_bf16", 8, 300, 98, "bf16", 33, dz_std=0.1),
+    Case("narrow2_hw49_f16", 32, 256, 49, "f16", 34, dz_std=0.1),
+    Case("narrow4_hw49_f32", 8, 2048, 49, "f32", 35),
+    Case("narrow8_hw14_f32", 16, 384, 14, "f32", 36),
+    Case("narrow2_bigchan_f16", 384, 256, 49, "f16", 37, dz_std=0.1),
+    Case("narrow4_rung256_bf16", 64, 300, 98, "bf16", 38, dz_std=0.1),
+    Case("narrow4_rung512_f16", 128, 256, 98, "f16", 39, dz_std=0.1),
 ]
 ALL_CASES = CONFIG_CASES + EDGE_CASES
 
@@ -295,12 +306,15 @@ def test_phases_equal_entry_on_streaming_shapes(case):
         assert torch.equal(getattr(A, k), getattr(B, k)), k
 
 
-@pytest.mark.parametrize("dtype,offset", [("f32", 16), ("f16", 8), ("bf16", 3), ("f32", 1)])
-def test_guard_band_and_alignment(dtype, offset):
+@pytest.mark.parametrize("dtype,offset,C", [("f32", 16, 6), ("f16", 8, 6), ("bf16", 3, 6), ("f32", 1, 6),
+                                            ("f16", 4, 256), ("bf16", 2, 256), ("f32", 2, 256),
+                                            ("f16", 1, 256)])
+def test_guard_band_and_alignment(dtype, offset, C):
     """Run inside a larger buffer: nothing outside [x, x+E) changes, and an
-    offset that breaks 16-byte alignment takes the one-element path with the
-    same results (to the parity tolerance)."""
-    case = Case("guard_%s_%d" % (dtype, offset), 3, 6, 800, dtype, 30)
+    offset that breaks 16-byte alignment takes a narrower access (8, 4 or 2
+    bytes; with C = 256 on the channel-resident kernels) with the same
+    results (to the parity tolerance)."""
+    case = Case("guard_%s_%d_c%d" % (dtype, offset, C), 3, C, 800, dtype, 30)
     inp = make_inputs(case)
     N, C, HW = case.N, case.C, case.HW
     E = N * C * HW
