@@ -149,10 +149,34 @@ struct alignas(16) Partial {
 
 __device__ __forceinline__ uint32_t lane_id() { return threadIdx.x & (kWave - 1); }
 
+// One DPP move of a double (both halves; lanes without a source read 0).
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ double dpp_f64(double v) {
+    const uint64_t bits = __builtin_bit_cast(uint64_t, v);
+    const int lo = __builtin_amdgcn_update_dpp(0, static_cast<int>(bits & 0xffffffffu), CTRL,
+                                               ROW_MASK, 0xF, true);
+    const int hi = __builtin_amdgcn_update_dpp(0, static_cast<int>(bits >> 32), CTRL, ROW_MASK,
+                                               0xF, true);
+    return __builtin_bit_cast(
+        double, (static_cast<uint64_t>(static_cast<uint32_t>(hi)) << 32) | static_cast<uint32_t>(lo));
+}
+
+// Sum over the 64 lanes of a wave (every lane must be active), returned in
+// every lane.  Register-to-register DPP steps: within each row of 16 lanes,
+// shifts by 1, 2, 4 and 8 leave the row's sum in its lane 15; two row
+// broadcasts then carry rows 0-1 and 2-3 into lane 63.  The order of the
+// additions is fixed, so the result is the same on every run.
 __device__ __forceinline__ double wave_sum(double v) {
-#pragma unroll
-    for (int off = kWave / 2; off > 0; off >>= 1) v += __shfl_down(v, off, kWave);
-    return v;  // valid in lane 0
+    v += dpp_f64<0x111, 0xF>(v);  // row_shr:1
+    v += dpp_f64<0x112, 0xF>(v);  // row_shr:2
+    v += dpp_f64<0x114, 0xF>(v);  // row_shr:4
+    v += dpp_f64<0x118, 0xF>(v);  // row_shr:8
+    v += dpp_f64<0x142, 0xA>(v);  // row_bcast:15 into rows 1 and 3
+    v += dpp_f64<0x143, 0xC>(v);  // row_bcast:31 into rows 2 and 3
+    const uint64_t bits = __builtin_bit_cast(uint64_t, v);
+    const uint32_t lo = __builtin_amdgcn_readlane(static_cast<int>(bits & 0xffffffffu), 63);
+    const uint32_t hi = __builtin_amdgcn_readlane(static_cast<int>(bits >> 32), 63);
+    return __builtin_bit_cast(double, (static_cast<uint64_t>(hi) << 32) | lo);
 }
 
 // Shifted sums re-expressed about another shift:
@@ -183,9 +207,9 @@ __device__ __forceinline__ void channel_moments(const Geom& g, const Partial* __
         s2 += t2;
         n += pq.d;
     }
-    s1 = __shfl(wave_sum(s1), 0, kWave);
-    s2 = __shfl(wave_sum(s2), 0, kWave);
-    n = __shfl(wave_sum(n), 0, kWave);
+    s1 = wave_sum(s1);
+    s2 = wave_sum(s2);
+    n = wave_sum(n);
     mean = kref + s1 / n;
     var = fmax(s2 - s1 * s1 / n, 0.0) / n;
 }
@@ -199,8 +223,8 @@ __device__ __forceinline__ void channel_sums(const Geom& g, const Partial* __res
         a += cp[q].a;
         b += cp[q].b;
     }
-    sdy = __shfl(wave_sum(a), 0, kWave);
-    sdyx = __shfl(wave_sum(b), 0, kWave);
+    sdy = wave_sum(a);
+    sdyx = wave_sum(b);
 }
 
 struct FwdParams {
