@@ -98,6 +98,7 @@ Geom make_geom(int64_t N, int64_t C, int64_t HW, int dtype, int vec) {
     g.row_div = iabn_divmagic_make(g.vrow);
     g.nstride = static_cast<uint64_t>(C) * g.vrow;
     g.m = static_cast<double>(m);
+    g.inv_m = 1.0 / g.m;
     return g;
 }
 

@@ -110,6 +110,7 @@ struct Geom {
     iabn_divmagic_t row_div;  // division by vrow
     uint64_t nstride;         // accesses between samples of a channel (C * vrow)
     double m;                 // elements per channel (N * HW)
+    double inv_m;             // 1 / m
 };
 
 // Index (in accesses) of the v-th access of channel c.
@@ -356,15 +357,30 @@ struct BwdApplyElem {
 
 // dgamma from the two sums (formulation II converts sum dy*y), then the
 // apply constants.  sdyw is overwritten with dgamma.
+// Reciprocals of the per-channel divisors, formed before the reduction so
+// that the constants after it take multiplications only.
+struct BwdRecip {
+    double g, ag, m;  // 1/gamma, 1/(slope gamma), 1/m
+};
+
+__device__ __forceinline__ BwdRecip make_recip(float gamma, float slope, double inv_m) {
+    const double g = gamma;
+    BwdRecip r;
+    r.g = 1.0 / g;
+    r.ag = 1.0 / (static_cast<double>(slope) * g);
+    r.m = inv_m;
+    return r;
+}
+
 template <int BM>
 __device__ __forceinline__ BwdApplyElem<BM> make_apply_elem(double A, double& sdyw, double dbeta,
-                                                            double m, float slope, float gamma,
-                                                            float beta, float mean, double invstd,
-                                                            bool ii) {
-    const double g = gamma, a = slope, bt = beta;
-    if (BM == kBwdFromZ && ii) sdyw = (sdyw - bt * dbeta) / g;
+                                                            const BwdRecip& rc, float slope,
+                                                            float gamma, float beta, float mean,
+                                                            double invstd, bool ii) {
+    const double a = slope, bt = beta;
+    if (BM == kBwdFromZ && ii) sdyw = (sdyw - bt * dbeta) * rc.g;
     const double dgamma = sdyw;
-    const double B = -A * dgamma / m, C = -A * dbeta / m;
+    const double B = -A * dgamma * rc.m, C = -A * dbeta * rc.m;
     BwdApplyElem<BM> el;
     el.sign.gamma = gamma;
     el.sign.beta = beta;
@@ -372,9 +388,9 @@ __device__ __forceinline__ BwdApplyElem<BM> make_apply_elem(double A, double& sd
     el.a_neg = static_cast<float>(A * a);
     el.off = 0.f;
     if constexpr (BM == kBwdFromZ) {
-        el.b_pos = static_cast<float>(B / g);
-        el.b_neg = static_cast<float>(B / (a * g));
-        el.c0 = static_cast<float>(C - B * bt / g);
+        el.b_pos = static_cast<float>(B * rc.g);
+        el.b_neg = static_cast<float>(B * rc.ag);
+        el.c0 = static_cast<float>(C - B * bt * rc.g);
     } else if constexpr (BM == kBwdFromXZ) {
         el.off = mean;
         el.b_pos = el.b_neg = static_cast<float>(B * invstd);
@@ -384,6 +400,13 @@ __device__ __forceinline__ BwdApplyElem<BM> make_apply_elem(double A, double& sd
         el.c0 = static_cast<float>(C);
     }
     return el;
+}
+
+// 1/sqrt(v) in double: the hardware estimate refined by one Newton step
+// (relative error about 1e-14, far below the fp32 constants it feeds).
+__device__ __forceinline__ double rsqrt_d(double v) {
+    const double r = __builtin_amdgcn_rsq(v);
+    return r * (1.5 - 0.5 * v * r * r);
 }
 
 struct BwdParams {

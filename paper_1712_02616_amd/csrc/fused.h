@@ -76,12 +76,17 @@ __device__ __forceinline__ void unpack(raw_t<DT, VEC> r, float (&v)[VEC]) {
 
 // Per-wave (shift, s1, s2, n) of a block, combined by wave 0 in a fixed
 // order into the channel's mean and biased variance.
+// Per-wave (shift, s1, s2, n) of a block, combined into the channel's mean
+// and biased variance.  Each wave writes its partial to LDS; after the one
+// barrier every wave combines all of them itself, in the same fixed order,
+// so all waves hold the same result without a second barrier.  inv_m is
+// 1/m for the block's m values (formed off the critical path).
 template <int T>
 __device__ __forceinline__ void block_moments(float shift, float s1, float s2, uint32_t nacc,
-                                              uint32_t vec, double& mean, double& var) {
+                                              uint32_t vec, double inv_m, double& mean,
+                                              double& var) {
     constexpr int W = T / kWave;
     __shared__ double red[W][4];
-    __shared__ double out[2];
     const double kw = __shfl(shift, 0, kWave);
     const double n = static_cast<double>(nacc) * vec;
     double d1 = s1, d2 = s2;
@@ -97,33 +102,25 @@ __device__ __forceinline__ void block_moments(float shift, float s1, float s2, u
         red[wave][3] = nw;
     }
     __syncthreads();
-    if (wave == 0) {
-        const double kref = red[0][0];
-        double t1 = 0.0, t2 = 0.0, tn = 0.0;
-        if (lane_id() < W) {
-            t1 = red[lane_id()][1];
-            t2 = red[lane_id()][2];
-            tn = red[lane_id()][3];
-            reshift(t1, t2, tn, red[lane_id()][0], kref);
-        }
-        t1 = wave_sum(t1);
-        t2 = wave_sum(t2);
-        tn = wave_sum(tn);
-        if (lane_id() == 0) {
-            out[0] = kref + t1 / tn;
-            out[1] = fmax(t2 - t1 * t1 / tn, 0.0) / tn;
-        }
+    const double kref = red[0][0];
+    double t1 = 0.0, t2 = 0.0;
+    if (lane_id() < W) {
+        double tn = red[lane_id()][3];
+        t1 = red[lane_id()][1];
+        t2 = red[lane_id()][2];
+        reshift(t1, t2, tn, red[lane_id()][0], kref);
     }
-    __syncthreads();
-    mean = out[0];
-    var = out[1];
+    t1 = wave_sum(t1);
+    t2 = wave_sum(t2);
+    mean = kref + t1 * inv_m;
+    var = fmax(t2 - t1 * t1 * inv_m, 0.0) * inv_m;
 }
 
+// Two sums over a block, returned in every thread (one barrier, as above).
 template <int T>
 __device__ __forceinline__ void block_sums(double a, double b, double& sa, double& sb) {
     constexpr int W = T / kWave;
     __shared__ double red[W][2];
-    __shared__ double out[2];
     a = wave_sum(a);
     b = wave_sum(b);
     const uint32_t wave = threadIdx.x / kWave;
@@ -132,19 +129,10 @@ __device__ __forceinline__ void block_sums(double a, double b, double& sa, doubl
         red[wave][1] = b;
     }
     __syncthreads();
-    if (wave == 0) {
-        double t1 = lane_id() < W ? red[lane_id()][0] : 0.0;
-        double t2 = lane_id() < W ? red[lane_id()][1] : 0.0;
-        t1 = wave_sum(t1);
-        t2 = wave_sum(t2);
-        if (lane_id() == 0) {
-            out[0] = t1;
-            out[1] = t2;
-        }
-    }
-    __syncthreads();
-    sa = out[0];
-    sb = out[1];
+    double t1 = lane_id() < W ? red[lane_id()][0] : 0.0;
+    double t2 = lane_id() < W ? red[lane_id()][1] : 0.0;
+    sa = wave_sum(t1);
+    sb = wave_sum(t2);
 }
 
 // Where each row of a channel holds a whole number of T-wide strips of

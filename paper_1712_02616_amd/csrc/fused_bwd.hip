@@ -33,6 +33,7 @@ __device__ __forceinline__ void bwd_fused_channel(const void* __restrict__ u,
         1.0 / sqrt(static_cast<double>(var_c) + static_cast<double>(prm.eps));
     const BwdReduceElem<BM> el =
         make_reduce_elem<BM>(prm.slope, gamma_c, beta_c, mean_c, invstd, prm.ii != 0);
+    const BwdRecip rc = make_recip(gamma_c, prm.slope, g.inv_m);
 
     // Register-resident accesses non-temporal, the rest cached (see
     // fwd_fused_channel).  kBwdFromXZ first loads z (into the registers x
@@ -168,7 +169,7 @@ __device__ __forceinline__ void bwd_fused_channel(const void* __restrict__ u,
 #pragma unroll
     for (int q = 0; q < NW; ++q) opaque(negm[q]);
     const double A = static_cast<double>(gamma_c) * invstd;
-    const BwdApplyElem<BM> dx_of = make_apply_elem<BM>(A, sdyw, dbeta, g.m, prm.slope, gamma_c,
+    const BwdApplyElem<BM> dx_of = make_apply_elem<BM>(A, sdyw, dbeta, rc, prm.slope, gamma_c,
                                                        beta_c, mean_c, invstd, prm.ii != 0);
     if (tid == 0) {
         prm.dgamma[c] = static_cast<float>(sdyw);

@@ -166,12 +166,12 @@ __device__ __forceinline__ void fwd_fused_channel(void* __restrict__ xz, const G
     }
 
     double mean, var;
-    block_moments<T>(shift, s1, s2, nacc, VEC, mean, var);
+    block_moments<T>(shift, s1, s2, nacc, VEC, g.inv_m, mean, var);
     uint32_t tid2 = tid;
     opaque(tid2);
 #pragma unroll
     for (int k = 0; k < R; ++k) opaque(keep[k]);
-    const double invstd = 1.0 / sqrt(var + static_cast<double>(prm.eps));
+    const double invstd = rsqrt_d(var + static_cast<double>(prm.eps));
     const double scale_d = FM == kFwdCkpt ? invstd : static_cast<double>(gamma_c) * invstd;
     const float mean_hi = static_cast<float>(mean);
     const double mean_lo = mean - static_cast<double>(mean_hi);

@@ -342,8 +342,9 @@ __global__ __launch_bounds__(kThreads) void bwd_apply_kernel(const void* __restr
     const double invstd = chan_invstd(prm, s.c);
     const double A = static_cast<double>(prm.gamma[s.c]) * invstd;
     const BwdApplyElem<BM> dx_of = make_apply_elem<BM>(
-        A, dgamma, dbeta, g.m, prm.slope, prm.gamma[s.c], prm.beta[s.c],
-        BM == kBwdFromXZ ? prm.save_mean[s.c] : 0.f, invstd, prm.ii != 0);
+        A, dgamma, dbeta, make_recip(prm.gamma[s.c], prm.slope, g.inv_m), prm.slope,
+        prm.gamma[s.c], prm.beta[s.c], BM == kBwdFromXZ ? prm.save_mean[s.c] : 0.f, invstd,
+        prm.ii != 0);
     if (s.p == 0 && threadIdx.x == 0) {
         prm.dgamma[s.c] = static_cast<float>(dgamma);
         prm.dbeta[s.c] = static_cast<float>(dbeta);
