@@ -296,6 +296,8 @@ def measure(lib, args):
         L.sm = torch.empty(C, device=dev)
         L.sv = torch.empty(C, device=dev)
         L.dg = torch.empty(C, device=dev)
+        L.rv0 = torch.zeros(C, device=dev)  # inference statistics: mean 0, variance 1
+        L.rv1 = torch.ones(C, device=dev)
         L.db = torch.empty(C, device=dev)
         p = lambda t: ctypes.c_void_p(t.data_ptr())  # noqa: E731
         L.fwd = (p(L.x), code, p(L.gamma), p(L.beta), p(L.rm), p(L.rv), p(L.sm), p(L.sv),
@@ -305,6 +307,8 @@ def measure(lib, args):
                  w.eps, w.slope, N, C, HW, wsp, ws_bytes, sp)
         L.reduce = (p(L.x), p(L.dz), code, p(L.gamma), p(L.beta), w.slope, N, C, HW, wsp,
                     ws_bytes, sp)
+        L.eval = (p(L.x), code, p(L.gamma), p(L.beta), p(L.rv0), p(L.rv1), w.eps, w.slope, N, C,
+                  HW, sp)
         layers.append(L)
     torch.cuda.synchronize()
     E_total = sum(L.E for L in layers)
@@ -380,6 +384,29 @@ def measure(lib, args):
                 "frac": round(k["achieved_gbps"] / HBM_PEAK_GBPS, 4),
                 "traffic": measured_traffic(dom, args.config)}
     log("entry points: " + json.dumps(kernels))
+
+    # ---------------------------------------------------------------- inference forward
+    # The inference forward (running statistics, in place) over the same
+    # layers: one read and one write per element.
+    refresh()
+    torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    for L in layers:
+        check(lib.iabn_forward_eval(*L.eval), "iabn_forward_eval")
+    ev[0].record(stream)
+    for i in range(args.steps):
+        for L in layers:
+            check(lib.iabn_forward_eval(*L.eval), "iabn_forward_eval")
+        ev[i + 1].record(stream)
+    torch.cuda.synchronize()
+    eval_ms = ev[0].elapsed_time(ev[-1])
+    kernels["iabn_forward_eval"] = {
+        "avg_us": round(eval_ms / launches * 1e3, 3), "launches": launches,
+        "alg_bytes_per_launch": 2 * E_total * b // len(layers),
+        "achieved_gbps": round(2 * E_total * b * args.steps / (eval_ms * 1e-3) / 1e9, 1),
+        "share_of_step": None}
+    log("inference forward: %.3f us per layer, %.1f GB/s" % (kernels["iabn_forward_eval"]["avg_us"],
+                                                             kernels["iabn_forward_eval"]["achieved_gbps"]))
 
     # ---------------------------------------------------------------- other blocks
     arms = None
