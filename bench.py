@@ -385,6 +385,28 @@ def measure(lib, args):
                 "traffic": measured_traffic(dom, args.config)}
     log("entry points: " + json.dumps(kernels))
 
+    # ---------------------------------------------------------------- copy reference
+    # A plain device-to-device copy of every layer's x and dz (torch's copy_,
+    # the runtime's copy kernel), chained over the same buffers: the same
+    # read-write mix and working set as the passes, with no arithmetic.
+    torch.cuda.synchronize()
+    c0 = torch.cuda.Event(enable_timing=True)
+    c1 = torch.cuda.Event(enable_timing=True)
+    reps = max(1, args.steps // 2)
+    c0.record(stream)
+    for _ in range(reps):
+        for L in layers:
+            L.x.copy_(L.x0)
+            L.dz.copy_(L.dz0)
+    c1.record(stream)
+    torch.cuda.synchronize()
+    copy_gbps = 2 * 2 * E_total * b * reps / (c0.elapsed_time(c1) * 1e-3) / 1e9
+    copy_ref = {"gbps": round(copy_gbps, 1),
+                "what": "device-to-device copy of every layer's x and dz (read + write), chained",
+                "iabn_forward_train_frac": round(kernels["iabn_forward_train"]["achieved_gbps"] / copy_gbps, 4),
+                "iabn_backward_frac": round(kernels["iabn_backward"]["achieved_gbps"] / copy_gbps, 4)}
+    log("copy reference: %.1f GB/s" % copy_gbps)
+
     # ---------------------------------------------------------------- inference forward
     # The inference forward (running statistics, in place) over the same
     # layers: one read and one write per element.
@@ -502,6 +524,7 @@ def measure(lib, args):
         "blocks": arms,
         "phase_kernels": phase_kernels,
         "roofline": roofline,
+        "copy_reference": copy_ref,
         "cpu_baseline": cpu,
     }
     return out
