@@ -251,7 +251,8 @@ def check_chain(dx, dgamma, dbeta, ref, allow, flip, dtype):
             name, np.nonzero(bad)[0][:5], got[bad][:5], r[bad][:5], slack[bad][:5])
 
 
-@pytest.mark.parametrize("case", [CONFIG_CASES[0], EDGE_CASES[0], EDGE_CASES[6], CONFIG_CASES[3]],
+@pytest.mark.parametrize("case", [CONFIG_CASES[0], EDGE_CASES[0], EDGE_CASES[6], CONFIG_CASES[3]] +
+                         [c for c in EDGE_CASES if c.id in ("narrow8_hw196_f16", "narrow4_hw98_bf16")],
                          ids=lambda c: c.id)
 def test_eval_parity(case):
     inp = make_inputs(case)
