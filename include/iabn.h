@@ -37,8 +37,14 @@
  *    of the scale-and-shift divides by gamma, Sec. 3.3 "Inversion of pi");
  *    gamma < 0 is allowed.  Buffers must not overlap except the documented
  *    in-place pairs.
+ *  - Tensor pointers need only the alignment of their element type.  Each
+ *    call reads and writes 16-byte accesses where HW and the pointers'
+ *    alignment allow, else 8-, 4- or 2-byte ones (a narrower access changes
+ *    the order of the sums, not the result beyond rounding).
  *  - Results are deterministic: the same inputs on the same device give
  *    bit-identical outputs (all reductions combine in a fixed order).
+ *  - The library keeps no device state between calls: calls on different
+ *    streams may run concurrently when they share no output or workspace.
  */
 #ifndef IABN_H
 #define IABN_H
