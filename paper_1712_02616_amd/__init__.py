@@ -131,10 +131,18 @@ def _stream(device, stream):
     return ctypes.c_void_p(int(stream))
 
 
-def _workspace(N, C, HW, code, device, workspace):
+def _workspace(N, C, HW, code, device, workspace, stream=None):
+    """The caller's workspace, or a new one from torch's caching allocator.
+    A new one is released when this call returns, while the kernels may still
+    run: the allocator reuses it only in the order of the stream it was
+    recorded on, so it is recorded on the stream the kernels run on."""
     need = iabn_workspace_size(N, C, HW, code)
     if workspace is None:
         workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=device)
+        if stream is not None:
+            if not isinstance(stream, torch.cuda.Stream):
+                stream = torch.cuda.ExternalStream(int(stream), device=device)
+            workspace.record_stream(stream)
     if workspace.device != device or not workspace.is_contiguous():
         raise ValueError("workspace must be a contiguous tensor on %s" % device)
     return workspace, ctypes.c_void_p(workspace.data_ptr()), workspace.numel() * workspace.element_size()
@@ -163,7 +171,7 @@ def iabn_forward_train(x_z, gamma, beta, running_mean, running_var, save_mean, s
     args = [_chan(t, C, dev, n) for t, n in ((gamma, "gamma"), (beta, "beta"),
             (running_mean, "running_mean"), (running_var, "running_var"),
             (save_mean, "save_mean"), (save_var, "save_var"))]
-    ws, wp, wb = _workspace(N, C, HW, code, dev, workspace)
+    ws, wp, wb = _workspace(N, C, HW, code, dev, workspace, stream)
     rc = load().iabn_forward_train(_ptr(x_z), code, *args, float(eps), float(momentum),
                                    float(slope), N, C, HW, wp, wb, _stream(dev, stream))
     _check("iabn_forward_train", rc)
@@ -194,7 +202,7 @@ def iabn_backward(z, dz_dx, gamma, beta, save_var, dgamma, dbeta, eps=1e-5, slop
     dev = z.device
     args = [_chan(t, C, dev, n) for t, n in ((gamma, "gamma"), (beta, "beta"),
             (save_var, "save_var"), (dgamma, "dgamma"), (dbeta, "dbeta"))]
-    ws, wp, wb = _workspace(N, C, HW, code, dev, workspace)
+    ws, wp, wb = _workspace(N, C, HW, code, dev, workspace, stream)
     rc = load().iabn_backward(_ptr(z), _ptr(dz_dx), code, *args, float(eps), float(slope), N, C, HW,
                               wp, wb, _stream(dev, stream))
     _check("iabn_backward", rc)
@@ -216,7 +224,7 @@ def iabn_backward_ii(z, dz_dx, gamma, beta, save_var, dgamma, dbeta, eps=1e-5, s
     dev = z.device
     args = [_chan(t, C, dev, n) for t, n in ((gamma, "gamma"), (beta, "beta"),
             (save_var, "save_var"), (dgamma, "dgamma"), (dbeta, "dbeta"))]
-    ws, wp, wb = _workspace(N, C, HW, code, dev, workspace)
+    ws, wp, wb = _workspace(N, C, HW, code, dev, workspace, stream)
     rc = load().iabn_backward_ii(_ptr(z), _ptr(dz_dx), code, *args, float(eps), float(slope), N, C,
                                  HW, wp, wb, _stream(dev, stream))
     _check("iabn_backward_ii", rc)
@@ -232,7 +240,7 @@ def iabn_std_forward_train(x, z, gamma, beta, running_mean, running_var, save_me
     args = [_chan(t, C, dev, n) for t, n in ((gamma, "gamma"), (beta, "beta"),
             (running_mean, "running_mean"), (running_var, "running_var"),
             (save_mean, "save_mean"), (save_var, "save_var"))]
-    ws, wp, wb = _workspace(N, C, HW, code, dev, workspace)
+    ws, wp, wb = _workspace(N, C, HW, code, dev, workspace, stream)
     rc = load().iabn_std_forward_train(_ptr(x), _ptr(z), code, *args, float(eps), float(momentum),
                                        float(slope), N, C, HW, wp, wb, _stream(dev, stream))
     _check("iabn_std_forward_train", rc)
@@ -248,7 +256,7 @@ def iabn_std_backward(x, z, dz_dx, gamma, beta, save_mean, save_var, dgamma, dbe
     dev = x.device
     args = [_chan(t, C, dev, n) for t, n in ((gamma, "gamma"), (beta, "beta"),
             (save_mean, "save_mean"), (save_var, "save_var"), (dgamma, "dgamma"), (dbeta, "dbeta"))]
-    ws, wp, wb = _workspace(N, C, HW, code, dev, workspace)
+    ws, wp, wb = _workspace(N, C, HW, code, dev, workspace, stream)
     rc = load().iabn_std_backward(_ptr(x), _ptr(z), _ptr(dz_dx), code, *args, float(eps),
                                   float(slope), N, C, HW, wp, wb, _stream(dev, stream))
     _check("iabn_std_backward", rc)
@@ -265,7 +273,7 @@ def iabn_ckpt_forward_train(x_xhat, z, gamma, beta, running_mean, running_var, s
     args = [_chan(t, C, dev, n) for t, n in ((gamma, "gamma"), (beta, "beta"),
             (running_mean, "running_mean"), (running_var, "running_var"),
             (save_mean, "save_mean"), (save_var, "save_var"))]
-    ws, wp, wb = _workspace(N, C, HW, code, dev, workspace)
+    ws, wp, wb = _workspace(N, C, HW, code, dev, workspace, stream)
     rc = load().iabn_ckpt_forward_train(_ptr(x_xhat), _ptr(z), code, *args, float(eps),
                                         float(momentum), float(slope), N, C, HW, wp, wb,
                                         _stream(dev, stream))
@@ -294,7 +302,7 @@ def iabn_ckpt_backward(xhat, dz_dx, gamma, beta, save_var, dgamma, dbeta, eps=1e
     dev = xhat.device
     args = [_chan(t, C, dev, n) for t, n in ((gamma, "gamma"), (beta, "beta"),
             (save_var, "save_var"), (dgamma, "dgamma"), (dbeta, "dbeta"))]
-    ws, wp, wb = _workspace(N, C, HW, code, dev, workspace)
+    ws, wp, wb = _workspace(N, C, HW, code, dev, workspace, stream)
     rc = load().iabn_ckpt_backward(_ptr(xhat), _ptr(dz_dx), code, *args, float(eps), float(slope),
                                    N, C, HW, wp, wb, _stream(dev, stream))
     _check("iabn_ckpt_backward", rc)
@@ -305,7 +313,7 @@ def iabn_forward_stats(x, workspace, stream=None):
     """First phase of the training forward: partial statistics into ``workspace``."""
     N, C, HW = _nchw(x, "x")
     code = DTYPE_CODES[x.dtype]
-    ws, wp, wb = _workspace(N, C, HW, code, x.device, workspace)
+    ws, wp, wb = _workspace(N, C, HW, code, x.device, workspace, stream)
     rc = load().iabn_forward_stats(_ptr(x), code, N, C, HW, wp, wb, _stream(x.device, stream))
     _check("iabn_forward_stats", rc)
 
@@ -319,7 +327,7 @@ def iabn_forward_apply(x_z, gamma, beta, running_mean, running_var, save_mean, s
     args = [_chan(t, C, dev, n) for t, n in ((gamma, "gamma"), (beta, "beta"),
             (running_mean, "running_mean"), (running_var, "running_var"),
             (save_mean, "save_mean"), (save_var, "save_var"))]
-    ws, wp, wb = _workspace(N, C, HW, code, dev, workspace)
+    ws, wp, wb = _workspace(N, C, HW, code, dev, workspace, stream)
     rc = load().iabn_forward_apply(_ptr(x_z), code, *args, float(eps), float(momentum),
                                    float(slope), N, C, HW, wp, wb, _stream(dev, stream))
     _check("iabn_forward_apply", rc)
@@ -335,7 +343,7 @@ def iabn_backward_reduce(z, dz, gamma, beta, slope, workspace, stream=None):
     dev = z.device
     g = _chan(gamma, C, dev, "gamma")
     b = _chan(beta, C, dev, "beta")
-    ws, wp, wb = _workspace(N, C, HW, code, dev, workspace)
+    ws, wp, wb = _workspace(N, C, HW, code, dev, workspace, stream)
     rc = load().iabn_backward_reduce(_ptr(z), _ptr(dz), code, g, b, float(slope), N, C, HW, wp, wb,
                                      _stream(dev, stream))
     _check("iabn_backward_reduce", rc)
@@ -351,7 +359,7 @@ def iabn_backward_apply(z, dz_dx, gamma, beta, save_var, dgamma, dbeta, eps, slo
     dev = z.device
     args = [_chan(t, C, dev, n) for t, n in ((gamma, "gamma"), (beta, "beta"),
             (save_var, "save_var"), (dgamma, "dgamma"), (dbeta, "dbeta"))]
-    ws, wp, wb = _workspace(N, C, HW, code, dev, workspace)
+    ws, wp, wb = _workspace(N, C, HW, code, dev, workspace, stream)
     rc = load().iabn_backward_apply(_ptr(z), _ptr(dz_dx), code, *args, float(eps), float(slope),
                                     N, C, HW, wp, wb, _stream(dev, stream))
     _check("iabn_backward_apply", rc)

@@ -83,9 +83,8 @@ size_t workspace_bytes_for(int64_t N, int64_t C, int64_t HW) {
     return static_cast<size_t>(C) * static_cast<size_t>(sp.P) * kWaves * sizeof(Partial);
 }
 
-
 // The access geometry for `vec` elements per access.
-Geom make_geom(int64_t N, int64_t C, int64_t HW, int dtype, int vec) {
+Geom make_geom(int64_t N, int64_t C, int64_t HW, int vec) {
     const int64_t m = N * HW;
     const Split sp = split_channel(m, C);
     Geom g;
@@ -175,7 +174,7 @@ int forward_train_impl(int fm, void* x, void* out, int dtype, const float* gamma
         return fail(IABN_ERR_PARAM, "momentum must lie in [0, 1]");
     if ((rc = check_workspace(N, C, HW, workspace, workspace_bytes))) return rc;
     const int vec = access_vec(HW, dtype, x, fm == kFwdInPlace ? nullptr : out, nullptr);
-    const Geom g = make_geom(N, C, HW, dtype, vec);
+    const Geom g = make_geom(N, C, HW, vec);
     const FwdParams prm = {gamma,    beta, running_mean, running_var, save_mean, save_var,
                            fm == kFwdInPlace ? nullptr : out, eps, momentum, slope};
     const hipStream_t st = static_cast<hipStream_t>(stream);
@@ -215,7 +214,7 @@ int backward_impl(int bm, bool ii, const void* u, const void* zs, void* dz_dx, i
     if ((rc = check_params(eps, slope))) return rc;
     if ((rc = check_workspace(N, C, HW, workspace, workspace_bytes))) return rc;
     const int vec = access_vec(HW, dtype, u, dz_dx, bm == kBwdFromXZ ? zs : nullptr);
-    const Geom g = make_geom(N, C, HW, dtype, vec);
+    const Geom g = make_geom(N, C, HW, vec);
     const BwdParams prm = {gamma, beta, save_mean, save_var, dgamma, dbeta, eps, slope, ii ? 1 : 0};
     const hipStream_t st = static_cast<hipStream_t>(stream);
     FusedPlan fp;
@@ -235,7 +234,6 @@ int backward_impl(int bm, bool ii, const void* u, const void* zs, void* dz_dx, i
 }  // namespace iabn_impl
 
 using namespace iabn_impl;
-
 
 // ---------------------------------------------------------------- C ABI
 
@@ -272,9 +270,9 @@ int iabn_forward_stats(const void* x, int dtype, int64_t N, int64_t C, int64_t H
     if (x == nullptr) return fail(IABN_ERR_NULL, "x is NULL");
     if ((rc = check_workspace(N, C, HW, workspace, workspace_bytes))) return rc;
     const int vec = access_vec(HW, dtype, x, nullptr, nullptr);
-    const Geom g = make_geom(N, C, HW, dtype, vec);
+    const Geom g = make_geom(N, C, HW, vec);
     launch_fwd_stats(dtype, vec, x, g, static_cast<Partial*>(workspace),
-                             static_cast<hipStream_t>(stream));
+                     static_cast<hipStream_t>(stream));
     return launched("fwd_stats");
 }
 
@@ -293,11 +291,11 @@ int iabn_forward_apply(void* x_z, int dtype, const float* gamma, const float* be
         return fail(IABN_ERR_PARAM, "momentum must lie in [0, 1]");
     if ((rc = check_workspace(N, C, HW, workspace, workspace_bytes))) return rc;
     const int vec = access_vec(HW, dtype, x_z, nullptr, nullptr);
-    const Geom g = make_geom(N, C, HW, dtype, vec);
+    const Geom g = make_geom(N, C, HW, vec);
     const FwdParams prm = {gamma, beta, running_mean, running_var, save_mean, save_var,
                            nullptr, eps, momentum, slope};
     launch_fwd_apply(dtype, vec, x_z, g, static_cast<const Partial*>(workspace), prm, true,
-                             kFwdInPlace, static_cast<hipStream_t>(stream));
+                     kFwdInPlace, static_cast<hipStream_t>(stream));
     return launched("fwd_apply");
 }
 
@@ -321,12 +319,12 @@ int iabn_forward_eval(void* x_z, int dtype, const float* gamma, const float* bet
         return fail(IABN_ERR_NULL, "a tensor or parameter pointer is NULL");
     if ((rc = check_params(eps, slope))) return rc;
     const int vec = access_vec(HW, dtype, x_z, nullptr, nullptr);
-    const Geom g = make_geom(N, C, HW, dtype, vec);
+    const Geom g = make_geom(N, C, HW, vec);
     const FwdParams prm = {gamma, beta, const_cast<float*>(running_mean),
                            const_cast<float*>(running_var), nullptr, nullptr, nullptr, eps, 0.f,
                            slope};
     launch_fwd_apply(dtype, vec, x_z, g, static_cast<const Partial*>(nullptr), prm, false,
-                             kFwdInPlace, static_cast<hipStream_t>(stream));
+                     kFwdInPlace, static_cast<hipStream_t>(stream));
     return launched("fwd_eval");
 }
 
@@ -342,11 +340,10 @@ int iabn_backward_reduce(const void* z, const void* dz, int dtype, const float* 
         return fail(IABN_ERR_PARAM, "slope must be finite and > 0 (the activation must be invertible)");
     if ((rc = check_workspace(N, C, HW, workspace, workspace_bytes))) return rc;
     const int vec = access_vec(HW, dtype, z, dz, nullptr);
-    const Geom g = make_geom(N, C, HW, dtype, vec);
+    const Geom g = make_geom(N, C, HW, vec);
     const BwdParams prm = {gamma, beta, nullptr, nullptr, nullptr, nullptr, 1.f, slope, 0};
-    launch_bwd_reduce(dtype, vec, z, static_cast<const void*>(nullptr), dz, g, prm,
-                              kBwdFromZ, static_cast<Partial*>(workspace),
-                              static_cast<hipStream_t>(stream));
+    launch_bwd_reduce(dtype, vec, z, static_cast<const void*>(nullptr), dz, g, prm, kBwdFromZ,
+                      static_cast<Partial*>(workspace), static_cast<hipStream_t>(stream));
     return launched("bwd_reduce");
 }
 
@@ -362,11 +359,11 @@ int iabn_backward_apply(const void* z, void* dz_dx, int dtype, const float* gamm
     if ((rc = check_params(eps, slope))) return rc;
     if ((rc = check_workspace(N, C, HW, workspace, workspace_bytes))) return rc;
     const int vec = access_vec(HW, dtype, z, dz_dx, nullptr);
-    const Geom g = make_geom(N, C, HW, dtype, vec);
+    const Geom g = make_geom(N, C, HW, vec);
     const BwdParams prm = {gamma, beta, nullptr, save_var, dgamma, dbeta, eps, slope, 0};
     launch_bwd_apply(dtype, vec, z, static_cast<const void*>(nullptr), dz_dx, g,
-                             static_cast<const Partial*>(workspace), prm, kBwdFromZ,
-                             static_cast<hipStream_t>(stream));
+                     static_cast<const Partial*>(workspace), prm, kBwdFromZ,
+                     static_cast<hipStream_t>(stream));
     return launched("bwd_apply");
 }
 
@@ -426,9 +423,8 @@ int iabn_ckpt_recompute(const void* xhat, void* z, int dtype, const float* gamma
         return fail(IABN_ERR_NULL, "a tensor or parameter pointer is NULL");
     if ((rc = check_params(1.f, slope))) return rc;
     const int vec = access_vec(HW, dtype, xhat, z, nullptr);
-    const Geom g = make_geom(N, C, HW, dtype, vec);
-    launch_recompute(dtype, vec, xhat, z, g, gamma, beta, slope,
-                              static_cast<hipStream_t>(stream));
+    const Geom g = make_geom(N, C, HW, vec);
+    launch_recompute(dtype, vec, xhat, z, g, gamma, beta, slope, static_cast<hipStream_t>(stream));
     return launched("recompute");
 }
 

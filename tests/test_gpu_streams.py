@@ -67,3 +67,47 @@ def test_two_streams_match_sequential():
     for L, r in zip(layers, ref):
         for k, v in r.items():
             assert torch.equal(L[k], v), k
+
+
+def test_side_stream_library_workspace():
+    """No workspace given and a stream that is not torch's current one: the
+    workspace the binding allocates is released when the call returns, while
+    the kernels still wait behind a long kernel on that stream; the current
+    stream allocates and overwrites blocks of the same size meanwhile, and the
+    results still match a plain run (the streaming kernels, which use the
+    workspace)."""
+    shape = (4, 24, 20008)
+    L = _layer(shape, "f32", 93)
+    nbytes = L["ws"].numel()
+    s0 = torch.cuda.current_stream()
+
+    def fresh():
+        L["x"] = L["x0"].clone()
+        L["dz"] = L["dz0"].clone()
+        L["rm"].fill_(0.0)
+        L["rv"].fill_(1.0)
+
+    say("side stream: reference")
+    fresh()
+    iabn.iabn_forward_train(L["x"], L["g"], L["b"], L["rm"], L["rv"], L["sm"], L["sv"])
+    iabn.iabn_backward(L["x"], L["dz"], L["g"], L["b"], L["sv"], L["dg"], L["db"])
+    torch.cuda.synchronize()
+    ref = {k: L[k].clone() for k in ("x", "dz", "rm", "rv", "sm", "sv", "dg", "db")}
+    say("side stream: library workspace")
+    side = torch.cuda.Stream()
+    for _ in range(3):
+        fresh()
+        side.wait_stream(s0)
+        with torch.cuda.stream(side):
+            torch.cuda._sleep(2_000_000)  # keeps the side stream busy for a while
+        iabn.iabn_forward_train(L["x"], L["g"], L["b"], L["rm"], L["rv"], L["sm"], L["sv"],
+                                stream=side)
+        junk = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+        junk.fill_(0xFF)
+        iabn.iabn_backward(L["x"], L["dz"], L["g"], L["b"], L["sv"], L["dg"], L["db"], stream=side)
+        junk = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+        junk.fill_(0x7F)
+        s0.wait_stream(side)
+        torch.cuda.synchronize()
+        for k, v in ref.items():
+            assert torch.equal(L[k], v), k
