@@ -401,23 +401,11 @@ def measure(lib, args):
     c1.record(stream)
     torch.cuda.synchronize()
     copy_gbps = 2 * 2 * E_total * b * reps / (c0.elapsed_time(c1) * 1e-3) / 1e9
-    # The backward's own mix, two reads and one write in place: torch's
-    # elementwise in-place add of every layer's x into its dz (the buffers
-    # are restored before they are used again).
-    c0.record(stream)
-    for _ in range(reps):
-        for L in layers:
-            L.dz.add_(L.x)
-    c1.record(stream)
-    torch.cuda.synchronize()
-    add_gbps = 3 * E_total * b * reps / (c0.elapsed_time(c1) * 1e-3) / 1e9
     copy_ref = {"gbps": round(copy_gbps, 1),
                 "what": "device-to-device copy of every layer's x and dz (read + write), chained",
                 "iabn_forward_train_frac": round(kernels["iabn_forward_train"]["achieved_gbps"] / copy_gbps, 4),
-                "two_reads_one_write_gbps": round(add_gbps, 1),
-                "two_reads_one_write_what": "in-place add of every layer's x into its dz, chained",
-                "iabn_backward_frac": round(kernels["iabn_backward"]["achieved_gbps"] / add_gbps, 4)}
-    log("copy reference: %.1f GB/s; in-place add (2 reads, 1 write): %.1f GB/s" % (copy_gbps, add_gbps))
+                "iabn_backward_frac": round(kernels["iabn_backward"]["achieved_gbps"] / copy_gbps, 4)}
+    log("copy reference: %.1f GB/s" % copy_gbps)
 
     # ---------------------------------------------------------------- inference forward
     # The inference forward (running statistics, in place) over the same
