@@ -142,6 +142,18 @@ class Layer:
     pass
 
 
+def cpu_model() -> str:
+    """The host CPU's model name (Linux), or "unknown"."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def time_arms(lib, layers, refresh, check, stream, args, E_total, b, iabn_kernels, dev, sp, code,
               w, wsp, ws_bytes):
     """The same step for the other blocks of Sec. 3.2, each through its own
@@ -484,7 +496,7 @@ def measure(lib, args):
         del f64
         passes = len(used) / len(order)
         cpu = {"value": round(done / spent, 1), "unit": "elements/s", "cores": oracle.num_threads(),
-               "kind": "oracle",
+               "kind": "oracle", "cpu_model": cpu_model(),
                "sample": "oracle fp64 forward_train + backward_i over %.2f passes of the %d layers "
                          "of %s, shape groups interleaved (%.3g elements, %.1f s of oracle time); "
                          "inputs converted to fp64 outside the timing" % (passes, len(order),
@@ -518,8 +530,12 @@ def measure(lib, args):
                 "two_pass_schedule_equivalent_gbps": round(sched_bytes / (ms_per_step * 1e-3) / 1e9, 1)},
         "event_ms_per_step": round(ev_ms_per_step, 4),
         "outputs_finite": finite,
-        "activation_memory": {"iabn_stored_bytes": E_total * b,
-                              "store_x_baseline_bytes": 2 * E_total * b},
+        # What the forward leaves for the backward: InPlace-ABN only the z
+        # buffers (the x buffers, overwritten), the standard block x and z.
+        # One workspace serves every layer and call.
+        "activation_memory": {"iabn_stored_bytes": sum(L.x.untyped_storage().nbytes() for L in layers),
+                              "store_x_baseline_bytes": 2 * E_total * b,
+                              "workspace_bytes": ws_bytes},
         "kernels": kernels,
         "blocks": arms,
         "phase_kernels": phase_kernels,
