@@ -1,5 +1,5 @@
 // Definitions shared by every kernel and the host side of libiabn:
-// storage types and 16-byte accesses, the access geometry of a layer, the
+// storage types and vector accesses, the access geometry of a layer, the
 // per-wave partial results of the streaming reductions, the parameters and
 // output modes of the forward, and the per-element forms of the backward
 // formulations.  InPlace-ABN (arXiv:1712.02616) for AMD Instinct MI355X
@@ -43,7 +43,7 @@ struct Elem<IABN_BF16> {
 constexpr int kCached = 0;
 constexpr int kStream = 1;
 
-// VEC elements per access: 16 bytes on the vector path, 1 on the scalar path.
+// VEC elements per access: 16, 8, 4 or 2 bytes, or a single element.
 template <int DT, int VEC, int HINT>
 __device__ __forceinline__ void load_vec(const void* __restrict__ base, uint64_t idx,
                                          float (&v)[VEC]) {
@@ -95,8 +95,6 @@ constexpr int kHintFwdApplyStore = kStream;
 constexpr int kHintReduceLoad = kCached;
 constexpr int kHintBwdApplyLoad = kStream;
 constexpr int kHintBwdApplyStore = kStream;
-// Apply passes visit the slices in reverse order of their reduction pass.
-constexpr bool kReverseApply = false;
 
 // ---------------------------------------------------------------- geometry
 
@@ -124,13 +122,10 @@ struct Slice {
     uint32_t c, p, lo, hi;
 };
 
-// REVERSE walks the slices from the last to the first: an apply pass then
-// starts on the data its reduction pass fetched most recently, which is the
-// data most likely still in the caches.
-template <bool REVERSE = false>
+// The slice of this block: blocks c*P .. c*P+P-1 cover channel c in order.
 __device__ __forceinline__ Slice block_slice(const Geom& g) {
     Slice s;
-    const uint32_t b = REVERSE ? gridDim.x - 1 - blockIdx.x : blockIdx.x;
+    const uint32_t b = blockIdx.x;
     s.c = b / g.P;
     s.p = b - s.c * g.P;
     s.lo = s.p * g.lv;
@@ -355,8 +350,6 @@ struct BwdApplyElem {
     }
 };
 
-// dgamma from the two sums (formulation II converts sum dy*y), then the
-// apply constants.  sdyw is overwritten with dgamma.
 // Reciprocals of the per-channel divisors, formed before the reduction so
 // that the constants after it take multiplications only.
 struct BwdRecip {
@@ -372,6 +365,8 @@ __device__ __forceinline__ BwdRecip make_recip(float gamma, float slope, double 
     return r;
 }
 
+// dgamma from the two sums (formulation II converts sum dy*y), then the
+// apply constants.  sdyw is overwritten with dgamma.
 template <int BM>
 __device__ __forceinline__ BwdApplyElem<BM> make_apply_elem(double A, double& sdyw, double dbeta,
                                                             const BwdRecip& rc, float slope,
@@ -423,6 +418,5 @@ struct BwdParams {
 __device__ __forceinline__ double chan_invstd(const BwdParams& prm, uint32_t c) {
     return 1.0 / sqrt(static_cast<double>(prm.save_var[c]) + static_cast<double>(prm.eps));
 }
-
 
 }  // namespace iabn_impl

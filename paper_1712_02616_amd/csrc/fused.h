@@ -1,4 +1,4 @@
-// Device helpers of the channel-resident (fused) kernels: raw 16-byte
+// Device helpers of the channel-resident (fused) kernels: raw access
 // registers, the block-level reductions of a channel, strip addressing, and
 // the optimiser barriers that keep the register-resident loops at their
 // register budget.
@@ -11,12 +11,12 @@
 namespace iabn_impl {
 
 // One block owns a whole channel and keeps the first R of each thread's
-// 16-byte accesses in registers between the reduction and the apply phase,
+// accesses in registers between the reduction and the apply phase,
 // so those bytes cross HBM once on the way in and once on the way out (the
 // forward reads x and writes z; the backward reads z and dz and writes dx).
 // Accesses beyond R (channels larger than the block's registers) are read
 // again in the apply phase.  Thread t handles accesses t, t + T, t + 2T, ...
-// of its channel, so a wave touches consecutive 16-byte vectors.  The only
+// of its channel, so a wave touches consecutive vectors.  The only
 // synchronisation is the block barrier around the channel's reduction.
 
 // One access of VEC elements of storage type DT, kept raw (undecoded) in
@@ -136,7 +136,7 @@ __device__ __forceinline__ void block_sums(double a, double b, double& sa, doubl
 }
 
 // Where each row of a channel holds a whole number of T-wide strips of
-// 16-byte accesses (vrow % T == 0) and the channel has at least R strips,
+// accesses (vrow % T == 0) and the channel has at least R strips,
 // access k of every thread of the block lies in strip k: its index is a
 // block-uniform strip offset plus the thread index, and every thread has an
 // access in each of the vchan / T strips.  The strip offsets are scalar

@@ -1,5 +1,5 @@
 // The channel-resident training forward: one block per channel holds the
-// channel's 16-byte accesses in registers from the statistics to the apply,
+// channel's accesses in registers from the statistics to the apply,
 // so x crosses HBM once in and the outputs once out.  Output modes as in
 // common.h (InPlace-ABN, standard, checkpointing).
 
@@ -16,7 +16,7 @@ struct FwdApplyK {
     void* out;                            // kFwdOut / kFwdCkpt: z
 };
 
-// The outputs of one 16-byte access from its input values t (overwritten).
+// The outputs of one access from its input values t (overwritten).
 template <int DT, int VEC, int FM, bool SMALL_SLOPE>
 __device__ __forceinline__ void fwd_fused_emit(void* __restrict__ xz, uint64_t idx,
                                                float (&t)[VEC], const FwdApplyK& k) {

@@ -29,12 +29,13 @@ void launch_recompute(int dtype, int vec, const void* xhat, void* z, const Geom&
 // ---- channel-resident kernels (fused_fwd.hip, fused_bwd.hip)
 
 // Used when every channel gets a block of its own and at least one block per
-// CU (C >= kFusedMinChannels) on the 16-byte path.
+// CU (C >= kFusedMinChannels): on the 16-byte path for every entry point,
+// on the narrower paths for InPlace-ABN's own forward and backward.
 constexpr int64_t kFusedMinChannels = 256;
 
 struct FusedPlan {
     int T;  // threads per block
-    int R;  // 16-byte accesses per thread held in registers (per tensor)
+    int R;  // accesses per thread held in registers (per tensor)
 };
 
 inline dim3 fused_grid(const Geom& g, const FusedPlan&) { return dim3(g.C); }

@@ -18,12 +18,12 @@
 // (channel, slice) pair, so each block sees a single channel and reads its
 // parameters once.  Slices are defined in elements, independent of the
 // access width, so the partials of a slice mean the same thing whichever
-// path wrote them.  Inside a slice a thread reads 16-byte vectors
-// v = lo + tid, lo + tid + 256, ... (consecutive lanes touch consecutive 16
-// bytes), U of them in flight before any arithmetic.  A vector never crosses
-// a row because HW is a multiple of the vector width on the vector path;
-// otherwise (odd HW, or a pointer not 16-byte aligned) the same kernels run
-// with one element per access.
+// path wrote them.  Inside a slice a thread reads vectors v = lo + tid,
+// lo + tid + 256, ... (consecutive lanes touch consecutive vectors), U of
+// them in flight before any arithmetic.  A vector is 16 bytes wide, or 8, 4
+// or 2 bytes where HW or the pointers' alignment rule out the wider ones, or
+// a single element (odd HW); it never crosses a row because HW is a multiple
+// of the vector width.
 //
 // In place.  Every element is read and then written by the same thread in
 // the same kernel, so x -> z and dz -> dx need no synchronisation between
@@ -122,7 +122,7 @@ template <int DT, int VEC, int U, bool TRAIN, int FM>
 __global__ __launch_bounds__(kThreads) void fwd_apply_kernel(void* __restrict__ xz, Geom g,
                                                              const Partial* __restrict__ part,
                                                              FwdParams prm) {
-    const Slice s = block_slice<kReverseApply>(g);
+    const Slice s = block_slice(g);
     const uint64_t cbase = static_cast<uint64_t>(s.c) * g.vrow;
 
     // First batch in flight before the per-channel coefficients are known.
@@ -320,7 +320,7 @@ __global__ __launch_bounds__(kThreads) void bwd_apply_kernel(const void* __restr
                                                              void* __restrict__ dzdx, Geom g,
                                                              const Partial* __restrict__ part,
                                                              BwdParams prm) {
-    const Slice s = block_slice<kReverseApply>(g);
+    const Slice s = block_slice(g);
     const uint64_t cbase = static_cast<uint64_t>(s.c) * g.vrow;
 
     uint32_t v = s.lo + threadIdx.x;
