@@ -268,7 +268,7 @@ bool launch_v(const void* u, const void* zs, void* dzdx, const Geom& g, const Fu
     const size_t lds = fused_lds(kFusedBwdBlocksPerCU);
     if constexpr (V * sizeof(typename Elem<DT>::T) == 16) {
         IABN_FUSED_CASE(256, 4)
-        IABN_FUSED_CASE(512, 4)
+        IABN_FUSED_CASE(256, 8)
         IABN_FUSED_CASE(256, 16)
         IABN_FUSED_CASE(512, 16)
         IABN_FUSED_CASE(1024, 11)

@@ -238,7 +238,7 @@ bool launch_v(void* xz, const Geom& g, const FusedPlan& fp, const FwdParams& prm
     const size_t lds = fused_lds(kFusedFwdBlocksPerCU);
     if constexpr (V * sizeof(typename Elem<DT>::T) == 16) {
         IABN_FUSED_CASE(256, 4)
-        IABN_FUSED_CASE(512, 4)
+        IABN_FUSED_CASE(256, 8)
         IABN_FUSED_CASE(256, 16)
         IABN_FUSED_CASE(512, 16)
         IABN_FUSED_CASE(1024, 16)

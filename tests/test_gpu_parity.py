@@ -90,6 +90,9 @@ EDGE_CASES = [
     Case("manych_c1300_bf16", 4, 1300, 8192, "bf16", 29, dz_std=0.1),
     Case("manych_c520_f32", 4, 520, 4096, "f32", 30, dz_std=0.1),
     Case("manych_t256_c512_f16", 16, 512, 2048, "f16", 31, dz_std=0.1),
+    # Channels of 1025-2048 accesses: the (256, 8) rung, strip-addressed.
+    Case("rung256x8_strip_f16", 8, 300, 2048, "f16", 40, dz_std=0.1, gamma_sign=True),
+    Case("rung256x8_strip_f32", 4, 264, 2048, "f32", 41),
     # Rows that are not a multiple of 16 bytes: the channel-resident kernels
     # with 8-, 4- and 2-byte accesses (14x14 and 7x7 maps, and the like),
     # including channels larger than the registers hold.
