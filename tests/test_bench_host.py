@@ -1,0 +1,51 @@
+"""Host-side logic of bench.py (no GPU): the one-GPU guard, and the rule that
+the measured HBM traffic is reported only for the kernel sources it was
+measured on."""
+
+from __future__ import annotations
+
+import os
+import subprocess
+import sys
+
+import bench
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def test_more_than_one_gpu_exits_with_a_message():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode != 0
+    assert "one GPU" in r.stderr
+    assert r.stdout == ""
+
+
+def _summary(tmp_path, digest, bwd=207427397, fwd=138284931):
+    p = tmp_path / "traffic.md"
+    p.write_text("# traffic\n\nsome text: not a field\n\n"
+                 "- source_sha256: `%s`\n"
+                 "- traffic_bytes_per_launch.iabn_backward: %d\n"
+                 "- traffic_bytes_per_launch.iabn_forward_train: %d\n" % (digest, bwd, fwd))
+    return str(p)
+
+
+def test_traffic_reported_for_matching_sources(tmp_path, monkeypatch):
+    monkeypatch.setattr(bench, "TRAFFIC_SUMMARY", _summary(tmp_path, bench.kernel_source_digest()))
+    assert bench.measured_traffic("iabn_backward", 5) == 207427397
+    assert bench.measured_traffic("iabn_forward_train", 5) == 138284931
+    assert bench.measured_traffic("iabn_forward_eval", 5) is None
+    # Only the workload the counters were taken on.
+    assert bench.measured_traffic("iabn_backward", 2) is None
+
+
+def test_traffic_withheld_for_other_sources(tmp_path, monkeypatch):
+    monkeypatch.setattr(bench, "TRAFFIC_SUMMARY", _summary(tmp_path, "0" * 64))
+    assert bench.measured_traffic("iabn_backward", 5) is None
+    monkeypatch.setattr(bench, "TRAFFIC_SUMMARY", str(tmp_path / "missing.md"))
+    assert bench.measured_traffic("iabn_backward", 5) is None
+
+
+def test_source_digest_covers_kernels_and_header():
+    d = bench.kernel_source_digest()
+    assert len(d) == 64 and d == bench.kernel_source_digest()
