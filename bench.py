@@ -11,7 +11,10 @@ through HBM the way a network does.
 
 Default workload: the ResNet-101-like backbone sweep (N=8, 512x512 input,
 output stride 8; 33 BN layers in four shape groups, fp16 storage, fp32
-arithmetic), 1.14e9 elements per tensor.
+arithmetic), 1.14e9 elements per tensor.  A workload whose x and dz together
+hold less than 1 GiB (the single-layer ones, --config 1-4) is replicated
+into distinct buffers up to that size (``config.replicas``), so that its
+passes read from HBM rather than from the 256 MB Infinity Cache.
 
 Output: one JSON line (see the keys below).  ``value`` is elements/s of the
 whole fwd+bwd step (elements = sum over layers of N*C*H*W).  ``kernels``
@@ -43,6 +46,9 @@ if ROOT not in sys.path:
 
 METRIC = "IABN fwd+bwd elements/s and achieved HBM GB/s (% of MI355X peak)"
 HBM_PEAK_GBPS = 8000.0
+# Working set (x and dz of every layer) below which a workload is replicated.
+REPLICA_BYTES = 1 << 30
+MAX_REPLICAS = 64
 
 # Algorithmic HBM bytes per element of each kernel, in units of the storage
 # size b: what the kernel must read and write once.
@@ -281,14 +287,19 @@ def measure(lib, args):
 
     # ---------------------------------------------------------------- inputs
     t0 = time.time()
-    host_layers = []
+    host_layers = [workloads.workload_layer(w, li) for li in range(len(w.layers))]
     layers = []
     ws_bytes = max(lib.iabn_workspace_size(n, c, hw, code) for n, c, hw in w.layers)
     workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
     wsp = ctypes.c_void_p(workspace.data_ptr())
-    for li, (N, C, HW) in enumerate(w.layers):
-        inp = workloads.workload_layer(w, li)
-        host_layers.append(inp)
+    # A workload whose x and dz fit in the Infinity Cache (the single-layer
+    # ones) is replicated into distinct buffers until they do not, so that
+    # every pass reads from HBM as in a network; each replica is a copy of
+    # the same synthetic input.
+    set_bytes = sum(2 * n * c * hw * b for n, c, hw in w.layers)
+    replicas = min(MAX_REPLICAS, max(1, -(-REPLICA_BYTES // set_bytes)))
+    for li, (N, C, HW) in [(li, shp) for _ in range(replicas) for li, shp in enumerate(w.layers)]:
+        inp = host_layers[li]
         L = Layer()
         L.shape = (N, C, HW)
         L.E = N * C * HW
@@ -517,6 +528,7 @@ def measure(lib, args):
         "dtype": "f32",
         "data": "synthetic (seeded, per-channel Gaussian activations, Gaussian gradients)",
         "config": {"workload": w.name, "storage": w.dtype, "layers": len(w.layers),
+                   "replicas": replicas,
                    "elements_per_tensor": E_total, "slope": w.slope, "eps": w.eps,
                    "momentum": w.momentum},
         # floor: every tensor crosses HBM once (x in, z out, z and dz in, dx
