@@ -406,6 +406,9 @@ def measure(lib, args):
                 "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                 "frac": round(k["achieved_gbps"] / HBM_PEAK_GBPS, 4),
                 "traffic": measured_traffic(dom, args.config)}
+    if roofline["traffic"]:
+        # The counted bytes over the same average launch duration.
+        roofline["traffic_gbps"] = round(roofline["traffic"] / (k["avg_us"] * 1e-6) / 1e9, 1)
     log("entry points: " + json.dumps(kernels))
 
     # ---------------------------------------------------------------- copy reference
