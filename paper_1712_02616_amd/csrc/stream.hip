@@ -416,10 +416,22 @@ constexpr int unroll() {
     return bytes >= 16 ? 2 : (32 / bytes < 8 ? 8 : 32 / bytes);
 }
 
+// The statistics pass over slices of at least 32 16-byte accesses per thread
+// keeps 8 loads in flight instead of 2 (read-only, so nothing else holds
+// registers): 15% faster on slices of 64K fp16 values, while shorter slices,
+// whose threads would leave most of a batch of 8 to the one-by-one remainder
+// loop, keep 2.
+constexpr uint32_t kLongSliceAccesses = 32 * kThreads;
+
 template <int DT, int VEC>
 struct LaunchFwdStats {
     static void run(const void* x, const Geom& g, Partial* part, hipStream_t st) {
-        fwd_stats_kernel<DT, VEC, unroll<DT, VEC>()><<<grid_of(g), kThreads, 0, st>>>(x, g, part);
+        constexpr int U = unroll<DT, VEC>();
+        constexpr bool wide = VEC * sizeof(typename Elem<DT>::T) == 16;
+        if (wide && g.lv >= kLongSliceAccesses)
+            fwd_stats_kernel<DT, VEC, wide ? 4 * U : U><<<grid_of(g), kThreads, 0, st>>>(x, g, part);
+        else
+            fwd_stats_kernel<DT, VEC, U><<<grid_of(g), kThreads, 0, st>>>(x, g, part);
     }
 };
 

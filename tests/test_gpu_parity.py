@@ -77,6 +77,9 @@ EDGE_CASES = [
     Case("ragged_slices_bf16", 3, 4, 20008, "bf16", 18, dz_std=0.1),
     Case("ragged_odd_f32", 4, 3, 12345, "f32", 19),
     Case("many_slices_f32", 2, 2, 1 << 20, "f32", 20, dz_std=0.1),
+    # Slices of 64K fp16 values on the streaming path (fewer than 256
+    # channels): the statistics pass with its deeper batches of loads.
+    Case("long_slices_f16", 8, 64, 65536, "f16", 42, dz_std=0.1),
     Case("all_negative_f16", 2, 8, 512, "f16", 21, beta_shift=-12.0),
     Case("all_positive_bf16", 2, 8, 512, "bf16", 22, beta_shift=12.0),
     Case("slope1_plain_bn_f32", 4, 8, 256, "f32", 23, slope=1.0),
