@@ -3,7 +3,7 @@
 addressing, access width from the row length and the pointers' alignment)
 exercised across shapes no hand-picked case names, each against the oracle
 with the gates of the other parity tests: InPlace-ABN's forward and backward
-(I and II), and the standard block's forward and backward.
+(I and II), the standard block's and the proposed checkpointing's.
 
 The shapes come from a fixed-seed generator, so every run tests the same
 list; a shape that fails is reproduced by its id.  Tensors sit at an element
@@ -203,4 +203,55 @@ def test_random_shape_standard_block(s):
     assert max_rel(to_f64(dg), bw["dgamma"]) <= TOL[s.dtype], "dgamma"
     assert max_rel(to_f64(db), bw["dbeta"]) <= TOL[s.dtype], "dbeta"
     for buf, fill in ((xbuf, 5.5), (zbuf, 1.75), (gbuf, -2.25)):
+        assert _untouched(buf, s.offset, E, fill)
+
+
+@pytest.mark.parametrize("s", SHAPES, ids=lambda s: s.id)
+def test_random_shape_checkpointing(s):
+    """The proposed checkpointing: forward (x̂ over x, z out of place; z
+    within the allowance of x̂'s storage rounding), recomputation equal to
+    the forward's z, and the backward from the stored x̂."""
+    from test_gpu_arms import assert_close_slack, ckpt_z_slack
+    eps, mom, slope = 1e-5, 0.1, 0.01
+    say("random checkpointing %s" % s.id)
+    inp = workloads.make_layer(s.N, s.C, s.HW, s.dtype, s.seed, dz_std=0.1, gamma_sign=True)
+    fw, _ = _stored(s, inp, eps, mom, slope)
+    E = s.N * s.C * s.HW
+    dev = torch.device("cuda")
+    gamma = torch.from_numpy(inp.gamma).to(dev)
+    beta = torch.from_numpy(inp.beta).to(dev)
+    rm = torch.from_numpy(inp.running_mean.copy()).to(dev)
+    rv = torch.from_numpy(inp.running_var.copy()).to(dev)
+    sm = torch.empty(s.C, device=dev)
+    sv = torch.empty(s.C, device=dev)
+    xbuf, xh = _placed(inp.x, s.dtype, s.offset, 5.5)
+    zbuf, z = _placed(np.zeros_like(inp.x), s.dtype, s.offset, 1.75)
+    iabn.iabn_ckpt_forward_train(xh, z, gamma, beta, rm, rv, sm, sv, eps, mom, slope)
+    torch.cuda.synchronize()
+    xh_ref = oracle.normalize(workloads.storage_to_f64(inp.x, s.dtype), fw["mean"], fw["var"], F32(eps))
+    assert_close("xhat", to_f64(xh), xh_ref, s.dtype)
+    assert_close_slack("z", to_f64(z), fw["z"], s.dtype, ckpt_z_slack(xh_ref, inp.gamma, slope, s.dtype))
+    for name, t in (("mean", sm), ("var", sv), ("running_mean", rm), ("running_var", rv)):
+        assert max_rel(to_f64(t), fw[name]) <= TOL["f32"], name
+    z2buf, z2 = _placed(np.zeros_like(inp.x), s.dtype, s.offset, 1.75)
+    iabn.iabn_ckpt_recompute(xh, z2, gamma, beta, slope)
+    torch.cuda.synchronize()
+    assert torch.equal(z2, z)
+    # Backward from the oracle's x̂ rounded to storage, on both sides.
+    var32 = fw["var"].astype(np.float32)
+    xh_store = workloads.f64_to_storage(xh_ref, s.dtype)
+    xh.copy_(to_device(xh_store, s.dtype))
+    gbuf, dz = _placed(inp.dz, s.dtype, s.offset, -2.25)
+    dg = torch.empty(s.C, device=dev)
+    db = torch.empty(s.C, device=dev)
+    iabn.iabn_ckpt_backward(xh, dz, gamma, beta, torch.from_numpy(var32).to(dev), dg, db, eps, slope)
+    torch.cuda.synchronize()
+    dz64 = workloads.storage_to_f64(inp.dz, s.dtype)
+    bw = oracle.backward_from_xhat(workloads.storage_to_f64(xh_store, s.dtype), dz64, inp.gamma,
+                                   inp.beta, var32, F32(eps), F32(slope))
+    A = np.abs(inp.gamma) / np.sqrt(var32.astype(np.float64) + F32(eps))
+    assert_close("dx", to_f64(dz), bw["dx"], s.dtype, floor_abs=1e-3 * float(A.max() * np.abs(dz64).max()))
+    assert max_rel(to_f64(dg), bw["dgamma"]) <= TOL[s.dtype], "dgamma"
+    assert max_rel(to_f64(db), bw["dbeta"]) <= TOL[s.dtype], "dbeta"
+    for buf, fill in ((xbuf, 5.5), (zbuf, 1.75), (z2buf, 1.75), (gbuf, -2.25)):
         assert _untouched(buf, s.offset, E, fill)
