@@ -96,6 +96,11 @@ EDGE_CASES = [
     # Channels of 1025-2048 accesses: the (256, 8) rung, strip-addressed.
     Case("rung256x8_strip_f16", 8, 300, 2048, "f16", 40, dz_std=0.1, gamma_sign=True),
     Case("rung256x8_strip_f32", 4, 264, 2048, "f32", 41),
+    # Fewer channels than CUs with channels that fit a block's registers: the
+    # channel-resident kernels from 64 channels (forward) and 96 (backward).
+    Case("fewch_c128_f16", 8, 128, 4096, "f16", 43, dz_std=0.1, gamma_sign=True),
+    Case("fewch_c96_bf16", 4, 96, 16384, "bf16", 44, dz_std=0.1),
+    Case("fewch_c64_f32", 16, 64, 1024, "f32", 45),
     # Rows that are not a multiple of 16 bytes: the channel-resident kernels
     # with 8-, 4- and 2-byte accesses (14x14 and 7x7 maps, and the like),
     # including channels larger than the registers hold.
