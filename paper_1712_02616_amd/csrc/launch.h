@@ -33,15 +33,23 @@ void launch_recompute(int dtype, int vec, const void* xhat, void* z, const Geom&
 // on the narrower paths for InPlace-ABN's own forward and backward.  With
 // fewer channels than CUs, a block per channel still beats the two passes of
 // the streaming kernels while the channel fits the largest block's registers
-// (or nearly, for the backward) and enough CUs get a channel: measured over
-// C = 64..256 and channels of 4K..64K accesses (fp16), from C = 64 for the
-// forward (C = 128, 16K accesses: 15 us against 25) and from C = 96 for the
-// backward (C = 128, 16K accesses: 27 us against 33); with larger channels,
-// or fewer, the streaming kernels are faster.
+// (or, from 128 channels, up to twice that) and enough CUs get a channel:
+// measured over C = 64..256 and channels of 4K..64K accesses, from C = 64
+// for the forward (C = 128, 16K accesses: 15 us against 25; 25K fp32
+// accesses: 25 against 31) and from C = 96 for the backward (C = 128, 16K
+// accesses: 27 us against 33); with larger channels, or fewer, the
+// streaming kernels are faster.
 constexpr int64_t kFusedMinChannels = 256;
 constexpr int64_t kFusedFewChannelsFwd = 64;
 constexpr int64_t kFusedFewChannelsBwd = 96;
+constexpr int64_t kFusedFewChannelsWide = 128;
 constexpr int64_t kFusedFewChannelsMaxAccesses = 16384;
+
+inline bool fused_few_channels_ok(int64_t C, uint32_t vchan, bool backward) {
+    if (C < (backward ? kFusedFewChannelsBwd : kFusedFewChannelsFwd)) return false;
+    const int64_t cap = kFusedFewChannelsMaxAccesses * (C >= kFusedFewChannelsWide ? 2 : 1);
+    return static_cast<int64_t>(vchan) <= cap;
+}
 
 struct FusedPlan {
     int T;  // threads per block
@@ -90,10 +98,7 @@ constexpr FusedPlan kNarrowLadder[] = {{256, 4}, {256, 8}, {256, 16}, {512, 16},
 // channel-resident kernels.
 inline bool plan_fused(int64_t C, const Geom& g, int elem_bytes, bool backward, bool narrow_ok,
                        FusedPlan* out) {
-    if (C < kFusedMinChannels &&
-        (C < (backward ? kFusedFewChannelsBwd : kFusedFewChannelsFwd) ||
-         static_cast<int64_t>(g.vchan) > kFusedFewChannelsMaxAccesses))
-        return false;
+    if (C < kFusedMinChannels && !fused_few_channels_ok(C, g.vchan, backward)) return false;
     const bool wide = static_cast<int>(g.vec) * elem_bytes == 16;
     if (!wide && !narrow_ok) return false;
     const FusedPlan* ladder = !wide ? kNarrowLadder : backward ? kBwdLadder : kFwdLadder;

@@ -101,6 +101,7 @@ EDGE_CASES = [
     Case("fewch_c128_f16", 8, 128, 4096, "f16", 43, dz_std=0.1, gamma_sign=True),
     Case("fewch_c96_bf16", 4, 96, 16384, "bf16", 44, dz_std=0.1),
     Case("fewch_c64_f32", 16, 64, 1024, "f32", 45),
+    Case("fewch_c128_big_f32", 8, 128, 12544, "f32", 46, dz_std=0.1),
     # Rows that are not a multiple of 16 bytes: the channel-resident kernels
     # with 8-, 4- and 2-byte accesses (14x14 and 7x7 maps, and the like),
     # including channels larger than the registers hold.
