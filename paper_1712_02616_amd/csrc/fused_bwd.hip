@@ -40,6 +40,13 @@ __device__ __forceinline__ void bwd_fused_channel(const void* __restrict__ u,
     // will use) and dz, turns z into sign bits, and only then loads x, so
     // that no more than two tensors' worth of registers is live.
     raw_t<DT, VEC> ku[R], kg[R];
+    // The first S accesses per thread past the registers (1024-thread blocks,
+    // whose registers hold 11 per tensor) wait in LDS from the reduction to
+    // the apply phase instead of being read again; each thread reads back
+    // only its own slots.  (Not for kBwdFromXZ, which would need a third
+    // tensor's worth.)
+    constexpr int S = (T == 1024 && !XZ) ? kBwdLdsAccesses : 0;
+    __shared__ raw_t<DT, VEC> lu[S > 0 ? S : 1][T], lg[S > 0 ? S : 1][T];
     uint32_t negm[NW];
 #pragma unroll
     for (int q = 0; q < NW; ++q) negm[q] = 0u;
@@ -146,15 +153,40 @@ __device__ __forceinline__ void bwd_fused_channel(const void* __restrict__ u,
         acc_dy += sdy;
         acc_dyw += sdyw;
     };
+    // The same for an access kept in LDS (read once: non-temporal).
+    auto accumulate_keep = [&](uint64_t i1, uint32_t slot) {
+        const raw_t<DT, VEC> ru = load_raw<DT, VEC, kStream>(u, i1);
+        const raw_t<DT, VEC> rg = load_raw<DT, VEC, kStream>(dzdx, i1);
+        lu[slot][tid] = ru;
+        lg[slot][tid] = rg;
+        float tu[VEC], tg[VEC];
+        unpack<DT, VEC>(ru, tu);
+        unpack<DT, VEC>(rg, tg);
+        float sdy = 0.f, sdyw = 0.f;
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) {
+            float dy, w;
+            el(tu[e], 0.f, tg[e], dy, w);
+            sdy += dy;
+            sdyw = fmaf(dy, w, sdyw);
+        }
+        acc_dy += sdy;
+        acc_dyw += sdyw;
+    };
     if constexpr (STRIP) {
 #pragma unroll 1
         for (uint32_t k = R; k < nstrips; ++k) {
-            accumulate(sp.off + tid);
+            if (S > 0 && k < R + S) accumulate_keep(sp.off + tid, k - R);
+            else accumulate(sp.off + tid);
             strip_next<T>(g, sp);
         }
     } else {
+        uint32_t j = 0;
 #pragma unroll 1
-        for (uint32_t v = tid + R * T; v < g.vchan; v += T) accumulate(access_index(g, cbase, v));
+        for (uint32_t v = tid + R * T; v < g.vchan; v += T, ++j) {
+            if (S > 0 && j < S) accumulate_keep(access_index(g, cbase, v), j);
+            else accumulate(access_index(g, cbase, v));
+        }
     }
 
     double dbeta, sdyw;
@@ -223,16 +255,23 @@ __device__ __forceinline__ void bwd_fused_channel(const void* __restrict__ u,
 #pragma unroll 1
         for (uint32_t k = R; k < nstrips; ++k) {
             const uint64_t i1 = sq.off + tid2;
-            emit(load_raw<DT, VEC, kStream>(u, i1), XZ ? load_raw<DT, VEC, kStream>(zs, i1) : zero16,
-                 load_raw<DT, VEC, kStream>(dzdx, i1), i1);
+            if (S > 0 && k < R + S)
+                emit(lu[k - R][tid2], zero16, lg[k - R][tid2], i1);
+            else
+                emit(load_raw<DT, VEC, kStream>(u, i1), XZ ? load_raw<DT, VEC, kStream>(zs, i1) : zero16,
+                     load_raw<DT, VEC, kStream>(dzdx, i1), i1);
             strip_next<T>(g, sq);
         }
     } else {
+        uint32_t j = 0;
 #pragma unroll 1
-        for (uint32_t v = tid2 + R * T; v < g.vchan; v += T) {
+        for (uint32_t v = tid2 + R * T; v < g.vchan; v += T, ++j) {
             const uint64_t i1 = access_index(g, cbase, v);
-            emit(load_raw<DT, VEC, kStream>(u, i1), XZ ? load_raw<DT, VEC, kStream>(zs, i1) : zero16,
-                 load_raw<DT, VEC, kStream>(dzdx, i1), i1);
+            if (S > 0 && j < S)
+                emit(lu[j][tid2], zero16, lg[j][tid2], i1);
+            else
+                emit(load_raw<DT, VEC, kStream>(u, i1), XZ ? load_raw<DT, VEC, kStream>(zs, i1) : zero16,
+                     load_raw<DT, VEC, kStream>(dzdx, i1), i1);
         }
     }
 }

@@ -39,9 +39,10 @@ __device__ __forceinline__ void fwd_fused_emit(void* __restrict__ xz, uint64_t i
 
 // Apply phase of the fused forward for the thread's resident accesses (from
 // registers) and the remainder (loaded again).
-template <int DT, int VEC, int T, int R, bool STRIP, int FM, bool SMALL_SLOPE>
+template <int DT, int VEC, int T, int R, int S, bool STRIP, int FM, bool SMALL_SLOPE>
 __device__ __forceinline__ void fwd_fused_apply(void* __restrict__ xz, const Geom& g, uint32_t c,
                                                 uint32_t tid, const raw_t<DT, VEC> (&keep)[R],
+                                                const raw_t<DT, VEC> (&lx)[S > 0 ? S : 1][T],
                                                 const FwdApplyK& kk) {
     const uint64_t cbase = static_cast<uint64_t>(c) * g.vrow;
     const uint32_t nstrips = STRIP ? g.vchan / T : 0;
@@ -71,16 +72,17 @@ __device__ __forceinline__ void fwd_fused_apply(void* __restrict__ xz, const Geo
         for (uint32_t k = R; k < nstrips; ++k) {
             const uint64_t idx = sq.off + tid;
             float t[VEC];
-            unpack<DT, VEC>(load_raw<DT, VEC, kStream>(xz, idx), t);
+            unpack<DT, VEC>(S > 0 && k < R + S ? lx[k - R][tid] : load_raw<DT, VEC, kStream>(xz, idx), t);
             fwd_fused_emit<DT, VEC, FM, SMALL_SLOPE>(xz, idx, t, kk);
             strip_next<T>(g, sq);
         }
     } else {
+        uint32_t j = 0;
 #pragma unroll 1
-        for (uint32_t v = tid + R * T; v < g.vchan; v += T) {
+        for (uint32_t v = tid + R * T; v < g.vchan; v += T, ++j) {
             const uint64_t idx = access_index(g, cbase, v);
             float t[VEC];
-            unpack<DT, VEC>(load_raw<DT, VEC, kStream>(xz, idx), t);
+            unpack<DT, VEC>(S > 0 && j < S ? lx[j][tid] : load_raw<DT, VEC, kStream>(xz, idx), t);
             fwd_fused_emit<DT, VEC, FM, SMALL_SLOPE>(xz, idx, t, kk);
         }
     }
@@ -109,6 +111,11 @@ __device__ __forceinline__ void fwd_fused_channel(void* __restrict__ xz, const G
     // register-resident loads cut the forward over the backbone sweep by 12%
     // and the backward by 7%.)
     raw_t<DT, VEC> keep[R];
+    // The first S accesses per thread past the registers (1024-thread
+    // blocks) wait in LDS for the apply phase instead of being read again;
+    // each thread reads back only its own slots.
+    constexpr int S = T == 1024 ? kFwdLdsAccesses : 0;
+    __shared__ raw_t<DT, VEC> lx[S > 0 ? S : 1][T];
     StripPos sp = strip_begin(g, c);
 #pragma unroll
     for (int k = 0; k < R; ++k) {
@@ -153,16 +160,28 @@ __device__ __forceinline__ void fwd_fused_channel(void* __restrict__ xz, const G
         }
         sched_fence();
     }
+    // Past the registers: kept in LDS (read once: non-temporal), or read
+    // again by the apply phase (through the caches).
+    auto accumulate_at = [&](uint64_t i1, uint32_t j) {
+        if (S > 0 && j < S) {
+            const raw_t<DT, VEC> r = load_raw<DT, VEC, kStream>(xz, i1);
+            lx[j][tid] = r;
+            accumulate(r);
+        } else {
+            accumulate(load_raw<DT, VEC, kCached>(xz, i1));
+        }
+    };
     if constexpr (STRIP) {
 #pragma unroll 1
         for (uint32_t k = R; k < nstrips; ++k) {
-            accumulate(load_raw<DT, VEC, kCached>(xz, sp.off + tid));
+            accumulate_at(sp.off + tid, k - R);
             strip_next<T>(g, sp);
         }
     } else {
+        uint32_t j = 0;
 #pragma unroll 1
-        for (uint32_t v = tid + R * T; v < g.vchan; v += T)
-            accumulate(load_raw<DT, VEC, kCached>(xz, access_index(g, cbase, v)));
+        for (uint32_t v = tid + R * T; v < g.vchan; v += T, ++j)
+            accumulate_at(access_index(g, cbase, v), j);
     }
 
     double mean, var;
@@ -197,9 +216,9 @@ __device__ __forceinline__ void fwd_fused_channel(void* __restrict__ xz, const G
     }
 
     if (kk.slope <= 1.f)
-        fwd_fused_apply<DT, VEC, T, R, STRIP, FM, true>(xz, g, c, tid2, keep, kk);
+        fwd_fused_apply<DT, VEC, T, R, S, STRIP, FM, true>(xz, g, c, tid2, keep, lx, kk);
     else
-        fwd_fused_apply<DT, VEC, T, R, STRIP, FM, false>(xz, g, c, tid2, keep, kk);
+        fwd_fused_apply<DT, VEC, T, R, S, STRIP, FM, false>(xz, g, c, tid2, keep, lx, kk);
 }
 
 // One block per channel: c = blockIdx.x.  (Giving each XCD a contiguous
