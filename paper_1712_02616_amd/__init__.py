@@ -18,6 +18,7 @@ from __future__ import annotations
 
 import ctypes
 import math
+import threading
 
 import torch
 
@@ -34,6 +35,7 @@ __all__ = [
 DTYPE_CODES = {torch.float32: 0, torch.float16: 1, torch.bfloat16: 2}
 
 _lib = None
+_lib_lock = threading.Lock()
 
 
 class IabnError(RuntimeError):
@@ -53,9 +55,11 @@ def load():
     global _lib
     if _lib is not None:
         return _lib
-    if not _build.is_built():
-        _build.build()
-    _lib = declare(ctypes.CDLL(_build.LIB))
+    with _lib_lock:
+        if _lib is None:
+            if not _build.is_built():
+                _build.build()
+            _lib = declare(ctypes.CDLL(_build.LIB))
     return _lib
 
 
