@@ -43,10 +43,10 @@ __device__ __forceinline__ void bwd_fused_channel(const void* __restrict__ u,
     // The first S accesses per thread past the registers (1024-thread blocks,
     // whose registers hold 11 per tensor) wait in LDS from the reduction to
     // the apply phase instead of being read again; each thread reads back
-    // only its own slots.  (Not for kBwdFromXZ, which would need a third
-    // tensor's worth.)
-    constexpr int S = (T == 1024 && !XZ) ? kBwdLdsAccesses : 0;
+    // only its own slots.  kBwdFromXZ keeps its third tensor (z) there too.
+    constexpr int S = T == 1024 ? (XZ ? kBwdLdsAccessesXZ : kBwdLdsAccesses) : 0;
     __shared__ raw_t<DT, VEC> lu[S > 0 ? S : 1][T], lg[S > 0 ? S : 1][T];
+    __shared__ raw_t<DT, VEC> lz[XZ && S > 0 ? S : 1][T];
     uint32_t negm[NW];
 #pragma unroll
     for (int q = 0; q < NW; ++q) negm[q] = 0u;
@@ -157,16 +157,24 @@ __device__ __forceinline__ void bwd_fused_channel(const void* __restrict__ u,
     auto accumulate_keep = [&](uint64_t i1, uint32_t slot) {
         const raw_t<DT, VEC> ru = load_raw<DT, VEC, kStream>(u, i1);
         const raw_t<DT, VEC> rg = load_raw<DT, VEC, kStream>(dzdx, i1);
+        float tu[VEC], tz[VEC], tg[VEC];
+        if constexpr (XZ) {
+            const raw_t<DT, VEC> rz = load_raw<DT, VEC, kStream>(zs, i1);
+            lz[slot][tid] = rz;
+            unpack<DT, VEC>(rz, tz);
+        } else {
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) tz[e] = 0.f;
+        }
         lu[slot][tid] = ru;
         lg[slot][tid] = rg;
-        float tu[VEC], tg[VEC];
         unpack<DT, VEC>(ru, tu);
         unpack<DT, VEC>(rg, tg);
         float sdy = 0.f, sdyw = 0.f;
 #pragma unroll
         for (int e = 0; e < VEC; ++e) {
             float dy, w;
-            el(tu[e], 0.f, tg[e], dy, w);
+            el(tu[e], tz[e], tg[e], dy, w);
             sdy += dy;
             sdyw = fmaf(dy, w, sdyw);
         }
@@ -256,7 +264,7 @@ __device__ __forceinline__ void bwd_fused_channel(const void* __restrict__ u,
         for (uint32_t k = R; k < nstrips; ++k) {
             const uint64_t i1 = sq.off + tid2;
             if (S > 0 && k < R + S)
-                emit(lu[k - R][tid2], zero16, lg[k - R][tid2], i1);
+                emit(lu[k - R][tid2], XZ ? lz[k - R][tid2] : zero16, lg[k - R][tid2], i1);
             else
                 emit(load_raw<DT, VEC, kStream>(u, i1), XZ ? load_raw<DT, VEC, kStream>(zs, i1) : zero16,
                      load_raw<DT, VEC, kStream>(dzdx, i1), i1);
@@ -268,7 +276,7 @@ __device__ __forceinline__ void bwd_fused_channel(const void* __restrict__ u,
         for (uint32_t v = tid2 + R * T; v < g.vchan; v += T, ++j) {
             const uint64_t i1 = access_index(g, cbase, v);
             if (S > 0 && j < S)
-                emit(lu[j][tid2], zero16, lg[j][tid2], i1);
+                emit(lu[j][tid2], XZ ? lz[j][tid2] : zero16, lg[j][tid2], i1);
             else
                 emit(load_raw<DT, VEC, kStream>(u, i1), XZ ? load_raw<DT, VEC, kStream>(zs, i1) : zero16,
                      load_raw<DT, VEC, kStream>(dzdx, i1), i1);

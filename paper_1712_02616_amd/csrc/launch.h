@@ -85,12 +85,14 @@ constexpr bool kUseStrips = true;
 
 // Accesses per thread past the registers that the 1024-thread blocks keep in
 // LDS (160 KB per CU, and such a block has the CU to itself): the forward 9
-// of x (144 KB), the backward 4 of each of its two tensors (128 KB).  Over
+// of x (144 KB), the backward 4 of each of its two tensors (128 KB; the
+// standard block's backward, which reads three, 3 of each: 144 KB).  Over
 // the backbone sweep's C = 256 layers this cut the backward from 39.3 to
 // 37.4 us (5 of 16 strips past the registers), on (32, 256, 56x56) fp32
 // from 67.0 to 61.9.
 constexpr int kFwdLdsAccesses = 9;
 constexpr int kBwdLdsAccesses = 4;
+constexpr int kBwdLdsAccessesXZ = 3;
 
 constexpr FusedPlan kFwdLadder[] = {{256, 4}, {256, 8}, {256, 16}, {512, 16}, {1024, 16}};
 constexpr FusedPlan kBwdLadder[] = {{256, 4}, {256, 8}, {256, 16}, {512, 16}, {1024, 11}};
