@@ -38,6 +38,7 @@ constexpr int64_t kTargetBlocks = 512;     // 2 blocks of 4 waves per CU on 256 
 constexpr int64_t kMinSliceElems = 4096;   // at least 16 elements per thread
 constexpr int64_t kMaxSlices = 1024;
 constexpr int64_t kSliceAlign = 8;         // slices start on a 16-byte access of any dtype
+constexpr int64_t kLineBytes = 128;        // L2 cache line
 
 int elem_bytes(int dtype) { return dtype == IABN_F32 ? 4 : 2; }
 
@@ -84,7 +85,7 @@ size_t workspace_bytes_for(int64_t N, int64_t C, int64_t HW) {
 }
 
 // The access geometry for `vec` elements per access.
-Geom make_geom(int64_t N, int64_t C, int64_t HW, int vec) {
+Geom make_geom(int64_t N, int64_t C, int64_t HW, int dtype, int vec) {
     const int64_t m = N * HW;
     const Split sp = split_channel(m, C);
     Geom g;
@@ -98,6 +99,9 @@ Geom make_geom(int64_t N, int64_t C, int64_t HW, int vec) {
     g.nstride = static_cast<uint64_t>(C) * g.vrow;
     g.m = static_cast<double>(m);
     g.inv_m = 1.0 / g.m;
+    g.xcd_order = (HW * elem_bytes(dtype)) % kLineBytes != 0 ? 1u : 0u;
+    g.xcd_q = static_cast<uint32_t>(C / kXcds);
+    g.xcd_r = static_cast<uint32_t>(C % kXcds);
     return g;
 }
 
@@ -174,7 +178,7 @@ int forward_train_impl(int fm, void* x, void* out, int dtype, const float* gamma
         return fail(IABN_ERR_PARAM, "momentum must lie in [0, 1]");
     if ((rc = check_workspace(N, C, HW, workspace, workspace_bytes))) return rc;
     const int vec = access_vec(HW, dtype, x, fm == kFwdInPlace ? nullptr : out, nullptr);
-    const Geom g = make_geom(N, C, HW, vec);
+    const Geom g = make_geom(N, C, HW, dtype, vec);
     const FwdParams prm = {gamma,    beta, running_mean, running_var, save_mean, save_var,
                            fm == kFwdInPlace ? nullptr : out, eps, momentum, slope};
     const hipStream_t st = static_cast<hipStream_t>(stream);
@@ -214,7 +218,7 @@ int backward_impl(int bm, bool ii, const void* u, const void* zs, void* dz_dx, i
     if ((rc = check_params(eps, slope))) return rc;
     if ((rc = check_workspace(N, C, HW, workspace, workspace_bytes))) return rc;
     const int vec = access_vec(HW, dtype, u, dz_dx, bm == kBwdFromXZ ? zs : nullptr);
-    const Geom g = make_geom(N, C, HW, vec);
+    const Geom g = make_geom(N, C, HW, dtype, vec);
     const BwdParams prm = {gamma, beta, save_mean, save_var, dgamma, dbeta, eps, slope, ii ? 1 : 0};
     const hipStream_t st = static_cast<hipStream_t>(stream);
     FusedPlan fp;
@@ -270,7 +274,7 @@ int iabn_forward_stats(const void* x, int dtype, int64_t N, int64_t C, int64_t H
     if (x == nullptr) return fail(IABN_ERR_NULL, "x is NULL");
     if ((rc = check_workspace(N, C, HW, workspace, workspace_bytes))) return rc;
     const int vec = access_vec(HW, dtype, x, nullptr, nullptr);
-    const Geom g = make_geom(N, C, HW, vec);
+    const Geom g = make_geom(N, C, HW, dtype, vec);
     launch_fwd_stats(dtype, vec, x, g, static_cast<Partial*>(workspace),
                      static_cast<hipStream_t>(stream));
     return launched("fwd_stats");
@@ -291,7 +295,7 @@ int iabn_forward_apply(void* x_z, int dtype, const float* gamma, const float* be
         return fail(IABN_ERR_PARAM, "momentum must lie in [0, 1]");
     if ((rc = check_workspace(N, C, HW, workspace, workspace_bytes))) return rc;
     const int vec = access_vec(HW, dtype, x_z, nullptr, nullptr);
-    const Geom g = make_geom(N, C, HW, vec);
+    const Geom g = make_geom(N, C, HW, dtype, vec);
     const FwdParams prm = {gamma, beta, running_mean, running_var, save_mean, save_var,
                            nullptr, eps, momentum, slope};
     launch_fwd_apply(dtype, vec, x_z, g, static_cast<const Partial*>(workspace), prm, true,
@@ -319,7 +323,7 @@ int iabn_forward_eval(void* x_z, int dtype, const float* gamma, const float* bet
         return fail(IABN_ERR_NULL, "a tensor or parameter pointer is NULL");
     if ((rc = check_params(eps, slope))) return rc;
     const int vec = access_vec(HW, dtype, x_z, nullptr, nullptr);
-    const Geom g = make_geom(N, C, HW, vec);
+    const Geom g = make_geom(N, C, HW, dtype, vec);
     const FwdParams prm = {gamma, beta, const_cast<float*>(running_mean),
                            const_cast<float*>(running_var), nullptr, nullptr, nullptr, eps, 0.f,
                            slope};
@@ -340,7 +344,7 @@ int iabn_backward_reduce(const void* z, const void* dz, int dtype, const float* 
         return fail(IABN_ERR_PARAM, "slope must be finite and > 0 (the activation must be invertible)");
     if ((rc = check_workspace(N, C, HW, workspace, workspace_bytes))) return rc;
     const int vec = access_vec(HW, dtype, z, dz, nullptr);
-    const Geom g = make_geom(N, C, HW, vec);
+    const Geom g = make_geom(N, C, HW, dtype, vec);
     const BwdParams prm = {gamma, beta, nullptr, nullptr, nullptr, nullptr, 1.f, slope, 0};
     launch_bwd_reduce(dtype, vec, z, static_cast<const void*>(nullptr), dz, g, prm, kBwdFromZ,
                       static_cast<Partial*>(workspace), static_cast<hipStream_t>(stream));
@@ -359,7 +363,7 @@ int iabn_backward_apply(const void* z, void* dz_dx, int dtype, const float* gamm
     if ((rc = check_params(eps, slope))) return rc;
     if ((rc = check_workspace(N, C, HW, workspace, workspace_bytes))) return rc;
     const int vec = access_vec(HW, dtype, z, dz_dx, nullptr);
-    const Geom g = make_geom(N, C, HW, vec);
+    const Geom g = make_geom(N, C, HW, dtype, vec);
     const BwdParams prm = {gamma, beta, nullptr, save_var, dgamma, dbeta, eps, slope, 0};
     launch_bwd_apply(dtype, vec, z, static_cast<const void*>(nullptr), dz_dx, g,
                      static_cast<const Partial*>(workspace), prm, kBwdFromZ,
@@ -423,7 +427,7 @@ int iabn_ckpt_recompute(const void* xhat, void* z, int dtype, const float* gamma
         return fail(IABN_ERR_NULL, "a tensor or parameter pointer is NULL");
     if ((rc = check_params(1.f, slope))) return rc;
     const int vec = access_vec(HW, dtype, xhat, z, nullptr);
-    const Geom g = make_geom(N, C, HW, vec);
+    const Geom g = make_geom(N, C, HW, dtype, vec);
     launch_recompute(dtype, vec, xhat, z, g, gamma, beta, slope, static_cast<hipStream_t>(stream));
     return launched("recompute");
 }

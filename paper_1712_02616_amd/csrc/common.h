@@ -109,7 +109,14 @@ struct Geom {
     uint64_t nstride;         // accesses between samples of a channel (C * vrow)
     double m;                 // elements per channel (N * HW)
     double inv_m;             // 1 / m
+    // Order of the channels over the blocks of a channel-resident launch
+    // (see fused_channel): xcd_order set, each XCD takes a contiguous range
+    // of channels, xcd_q or xcd_q + 1 of them.
+    uint32_t xcd_order, xcd_q, xcd_r;
 };
+
+// XCDs (accelerator complex dies, each with its own L2) of the device.
+constexpr uint32_t kXcds = 8;
 
 // Index (in accesses) of the v-th access of channel c.
 __device__ __forceinline__ uint64_t access_index(const Geom& g, uint64_t cbase, uint32_t v) {

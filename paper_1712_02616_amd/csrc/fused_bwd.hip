@@ -290,7 +290,7 @@ __global__ __launch_bounds__(T) void bwd_fused_kernel(const void* __restrict__ u
                                                       const void* __restrict__ zs,
                                                       void* __restrict__ dzdx, Geom g,
                                                       BwdParams prm) {
-    bwd_fused_channel<DT, VEC, T, R, STRIP, BM>(u, zs, dzdx, g, prm, blockIdx.x);
+    bwd_fused_channel<DT, VEC, T, R, STRIP, BM>(u, zs, dzdx, g, prm, fused_channel(g, blockIdx.x));
 }
 
 #define IABN_FUSED_CASE(TT, RR)                                                              \

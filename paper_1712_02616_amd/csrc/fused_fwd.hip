@@ -232,7 +232,7 @@ __device__ __forceinline__ void fwd_fused_channel(void* __restrict__ xz, const G
 template <int DT, int VEC, int T, int R, bool STRIP, int FM>
 __global__ __launch_bounds__(T) void fwd_fused_kernel(void* __restrict__ xz, Geom g,
                                                       FwdParams prm) {
-    fwd_fused_channel<DT, VEC, T, R, STRIP, FM>(xz, g, prm, blockIdx.x);
+    fwd_fused_channel<DT, VEC, T, R, STRIP, FM>(xz, g, prm, fused_channel(g, blockIdx.x));
 }
 
 #define IABN_FUSED_CASE(TT, RR)                                                              \
