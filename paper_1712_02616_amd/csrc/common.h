@@ -109,9 +109,10 @@ struct Geom {
     uint64_t nstride;         // accesses between samples of a channel (C * vrow)
     double m;                 // elements per channel (N * HW)
     double inv_m;             // 1 / m
-    // Order of the channels over the blocks of a channel-resident launch
-    // (see fused_channel): xcd_order set, each XCD takes a contiguous range
-    // of channels, xcd_q or xcd_q + 1 of them.
+    // Order of the channels (or slices) over the blocks of a launch (see
+    // fused_channel and block_slice): xcd_order set, each XCD takes a
+    // contiguous range of them; a channel-resident launch's XCDs take xcd_q
+    // or xcd_q + 1 channels each.
     uint32_t xcd_order, xcd_q, xcd_r;
 };
 
@@ -129,10 +130,19 @@ struct Slice {
     uint32_t c, p, lo, hi;
 };
 
-// The slice of this block: blocks c*P .. c*P+P-1 cover channel c in order.
+// The slice of this block: slice k = c*P + p covers part p of channel c.
+// Block k takes slice k, or, with xcd_order (rows that do not end on a
+// cache line), the blocks on each XCD (block b on XCD b mod 8) take a
+// contiguous range of slices, so that neighbouring slices, which share the
+// lines where their rows meet, read them through one L2 (the inference
+// forward on (32, 2048, 7x7) fp16: 10.2 us against 14.5).
 __device__ __forceinline__ Slice block_slice(const Geom& g) {
     Slice s;
-    const uint32_t b = blockIdx.x;
+    uint32_t b = blockIdx.x;
+    if (g.xcd_order) {
+        const uint32_t n = gridDim.x, x = b % kXcds, j = b / kXcds;
+        b = x * (n / kXcds) + min(x, n % kXcds) + j;
+    }
     s.c = b / g.P;
     s.p = b - s.c * g.P;
     s.lo = s.p * g.lv;
