@@ -80,28 +80,18 @@ __global__ __launch_bounds__(kThreads) void fwd_stats_kernel(const void* __restr
         s2 += a2;
         nacc += U;
     }
-    // The remainder, fewer than U accesses per thread: one batch, all loads
-    // in flight, then the sums one access at a time.
-    {
-        float t[U][VEC];
+    for (; v < s.hi; v += kThreads) {
+        float t[VEC];
+        load_vec<DT, VEC, kHintStatsLoad>(x, access_index(g, cbase, v), t);
+        if (first) shift = t[0];
+        first = false;
 #pragma unroll
-        for (int q = 0; q < U; ++q)
-            if (v + q * kThreads < s.hi)
-                load_vec<DT, VEC, kHintStatsLoad>(x, access_index(g, cbase, v + q * kThreads), t[q]);
-#pragma unroll
-        for (int q = 0; q < U; ++q) {
-            if (v + q * kThreads < s.hi) {
-                if (first) shift = t[q][0];
-                first = false;
-#pragma unroll
-                for (int k = 0; k < VEC; ++k) {
-                    const float d = t[q][k] - shift;
-                    s1 += d;
-                    s2 = fmaf(d, d, s2);
-                }
-                nacc += 1;
-            }
+        for (int k = 0; k < VEC; ++k) {
+            const float d = t[k] - shift;
+            s1 += d;
+            s2 = fmaf(d, d, s2);
         }
+        nacc += 1;
     }
     // Lane 0 has the smallest index of its wave, so if it read nothing the
     // whole wave read nothing and its sums are zero.
@@ -135,23 +125,18 @@ __global__ __launch_bounds__(kThreads) void fwd_apply_kernel(void* __restrict__ 
     const Slice s = block_slice(g);
     const uint64_t cbase = static_cast<uint64_t>(s.c) * g.vrow;
 
-    // Batches of U accesses per thread, the last one partial, all of a
-    // batch's loads in flight before its stores; the first batch is in
-    // flight before the per-channel coefficients are known.
+    // First batch in flight before the per-channel coefficients are known.
     uint32_t v = s.lo + threadIdx.x;
     float t[U][VEC];
     uint64_t idx[U];
-    auto load_batch = [&]() {
+    bool full = v + (U - 1) * kThreads < s.hi;
+    if (full) {
 #pragma unroll
         for (int q = 0; q < U; ++q) {
-            if (v + q * kThreads < s.hi) {
-                idx[q] = access_index(g, cbase, v + q * kThreads);
-                load_vec<DT, VEC, kHintFwdApplyLoad>(xz, idx[q], t[q]);
-            }
+            idx[q] = access_index(g, cbase, v + q * kThreads);
+            load_vec<DT, VEC, kHintFwdApplyLoad>(xz, idx[q], t[q]);
         }
-    };
-    bool more = v < s.hi;
-    if (more) load_batch();
+    }
 
     double mean, var;
     if constexpr (TRAIN) {
@@ -201,19 +186,30 @@ __global__ __launch_bounds__(kThreads) void fwd_apply_kernel(void* __restrict__ 
         }
     };
 
-    while (more) {
+    while (full) {
 #pragma unroll
-        for (int q = 0; q < U; ++q)
-            if (v + q * kThreads < s.hi) emit(t[q], idx[q]);
+        for (int q = 0; q < U; ++q) emit(t[q], idx[q]);
         v += U * kThreads;
-        more = v < s.hi;
-        if (more) load_batch();
+        full = v + (U - 1) * kThreads < s.hi;
+        if (full) {
+#pragma unroll
+            for (int q = 0; q < U; ++q) {
+                idx[q] = access_index(g, cbase, v + q * kThreads);
+                load_vec<DT, VEC, kHintFwdApplyLoad>(xz, idx[q], t[q]);
+            }
+        }
+    }
+    for (; v < s.hi; v += kThreads) {
+        float r[VEC];
+        const uint64_t i1 = access_index(g, cbase, v);
+        load_vec<DT, VEC, kHintFwdApplyLoad>(xz, i1, r);
+        emit(r, i1);
     }
 }
 
 // z = f(gamma * xhat + beta) from a stored xhat, out of place: the
 // recomputation step of the proposed checkpointing (Fig. 2(c)).
-template <int DT, int VEC, int U>
+template <int DT, int VEC>
 __global__ __launch_bounds__(kThreads) void recompute_kernel(const void* __restrict__ xhat,
                                                              void* __restrict__ z, Geom g,
                                                              const float* __restrict__ gamma,
@@ -222,29 +218,16 @@ __global__ __launch_bounds__(kThreads) void recompute_kernel(const void* __restr
     const Slice s = block_slice(g);
     const uint64_t cbase = static_cast<uint64_t>(s.c) * g.vrow;
     const float gm = gamma[s.c], bt = beta[s.c];
-    // Batches of U accesses per thread (the last one partial), all of a
-    // batch's loads in flight before its stores.
-    for (uint32_t v = s.lo + threadIdx.x; v < s.hi; v += U * kThreads) {
-        float r[U][VEC];
-        uint64_t idx[U];
+    for (uint32_t v = s.lo + threadIdx.x; v < s.hi; v += kThreads) {
+        float r[VEC];
+        const uint64_t i1 = access_index(g, cbase, v);
+        load_vec<DT, VEC, kStream>(xhat, i1, r);
 #pragma unroll
-        for (int q = 0; q < U; ++q) {
-            if (v + q * kThreads < s.hi) {
-                idx[q] = access_index(g, cbase, v + q * kThreads);
-                load_vec<DT, VEC, kStream>(xhat, idx[q], r[q]);
-            }
+        for (int k = 0; k < VEC; ++k) {
+            const float y = fmaf(r[k], gm, bt);
+            r[k] = y >= 0.f ? y : slope * y;
         }
-#pragma unroll
-        for (int q = 0; q < U; ++q) {
-            if (v + q * kThreads < s.hi) {
-#pragma unroll
-                for (int k = 0; k < VEC; ++k) {
-                    const float y = fmaf(r[q][k], gm, bt);
-                    r[q][k] = y >= 0.f ? y : slope * y;
-                }
-                store_vec<DT, VEC, kStream>(z, idx[q], r[q]);
-            }
-        }
+        store_vec<DT, VEC, kStream>(z, i1, r);
     }
 }
 
@@ -300,34 +283,22 @@ __global__ __launch_bounds__(kThreads) void bwd_reduce_kernel(const void* __rest
         acc_dy += sdy;
         acc_dyw += sdyw;
     }
-    // The remainder, fewer than U accesses per thread: one batch, all loads
-    // in flight, then the sums one access at a time.
-    {
-        float tu[U][VEC], tz[U][VEC], tg[U][VEC];
+    for (; v < s.hi; v += kThreads) {
+        float tu[VEC], tz[VEC], tg[VEC];
+        const uint64_t i1 = access_index(g, cbase, v);
+        load_vec<DT, VEC, kHintReduceLoad>(u, i1, tu);
+        load_sign<DT, VEC, kHintReduceLoad, BM>(zs, i1, tz);
+        load_vec<DT, VEC, kHintReduceLoad>(dz, i1, tg);
+        float sdy = 0.f, sdyw = 0.f;
 #pragma unroll
-        for (int q = 0; q < U; ++q) {
-            if (v + q * kThreads < s.hi) {
-                const uint64_t i1 = access_index(g, cbase, v + q * kThreads);
-                load_vec<DT, VEC, kHintReduceLoad>(u, i1, tu[q]);
-                load_sign<DT, VEC, kHintReduceLoad, BM>(zs, i1, tz[q]);
-                load_vec<DT, VEC, kHintReduceLoad>(dz, i1, tg[q]);
-            }
+        for (int k = 0; k < VEC; ++k) {
+            float dy, w;
+            el(tu[k], tz[k], tg[k], dy, w);
+            sdy += dy;
+            sdyw = fmaf(dy, w, sdyw);
         }
-#pragma unroll
-        for (int q = 0; q < U; ++q) {
-            if (v + q * kThreads < s.hi) {
-                float sdy = 0.f, sdyw = 0.f;
-#pragma unroll
-                for (int k = 0; k < VEC; ++k) {
-                    float dy, w;
-                    el(tu[q][k], tz[q][k], tg[q][k], dy, w);
-                    sdy += dy;
-                    sdyw = fmaf(dy, w, sdyw);
-                }
-                acc_dy += sdy;
-                acc_dyw += sdyw;
-            }
-        }
+        acc_dy += sdy;
+        acc_dyw += sdyw;
     }
     acc_dy = wave_sum(acc_dy);
     acc_dyw = wave_sum(acc_dyw);
@@ -352,23 +323,19 @@ __global__ __launch_bounds__(kThreads) void bwd_apply_kernel(const void* __restr
     const Slice s = block_slice(g);
     const uint64_t cbase = static_cast<uint64_t>(s.c) * g.vrow;
 
-    // Batches as in fwd_apply_kernel.
     uint32_t v = s.lo + threadIdx.x;
     float tu[U][VEC], tz[U][VEC], tg[U][VEC];
     uint64_t idx[U];
-    auto load_batch = [&]() {
+    bool full = v + (U - 1) * kThreads < s.hi;
+    if (full) {
 #pragma unroll
         for (int q = 0; q < U; ++q) {
-            if (v + q * kThreads < s.hi) {
-                idx[q] = access_index(g, cbase, v + q * kThreads);
-                load_vec<DT, VEC, kHintBwdApplyLoad>(u, idx[q], tu[q]);
-                load_sign<DT, VEC, kHintBwdApplyLoad, BM>(zs, idx[q], tz[q]);
-                load_vec<DT, VEC, kHintBwdApplyLoad>(dzdx, idx[q], tg[q]);
-            }
+            idx[q] = access_index(g, cbase, v + q * kThreads);
+            load_vec<DT, VEC, kHintBwdApplyLoad>(u, idx[q], tu[q]);
+            load_sign<DT, VEC, kHintBwdApplyLoad, BM>(zs, idx[q], tz[q]);
+            load_vec<DT, VEC, kHintBwdApplyLoad>(dzdx, idx[q], tg[q]);
         }
-    };
-    bool more = v < s.hi;
-    if (more) load_batch();
+    }
 
     double dbeta, dgamma;
     channel_sums(g, part, s.c, dbeta, dgamma);
@@ -383,18 +350,34 @@ __global__ __launch_bounds__(kThreads) void bwd_apply_kernel(const void* __restr
         prm.dbeta[s.c] = static_cast<float>(dbeta);
     }
 
-    while (more) {
+    while (full) {
 #pragma unroll
         for (int q = 0; q < U; ++q) {
-            if (v + q * kThreads < s.hi) {
 #pragma unroll
-                for (int k = 0; k < VEC; ++k) tg[q][k] = dx_of(tu[q][k], tz[q][k], tg[q][k]);
-                store_vec<DT, VEC, kHintBwdApplyStore>(dzdx, idx[q], tg[q]);
-            }
+            for (int k = 0; k < VEC; ++k) tg[q][k] = dx_of(tu[q][k], tz[q][k], tg[q][k]);
+            store_vec<DT, VEC, kHintBwdApplyStore>(dzdx, idx[q], tg[q]);
         }
         v += U * kThreads;
-        more = v < s.hi;
-        if (more) load_batch();
+        full = v + (U - 1) * kThreads < s.hi;
+        if (full) {
+#pragma unroll
+            for (int q = 0; q < U; ++q) {
+                idx[q] = access_index(g, cbase, v + q * kThreads);
+                load_vec<DT, VEC, kHintBwdApplyLoad>(u, idx[q], tu[q]);
+                load_sign<DT, VEC, kHintBwdApplyLoad, BM>(zs, idx[q], tz[q]);
+                load_vec<DT, VEC, kHintBwdApplyLoad>(dzdx, idx[q], tg[q]);
+            }
+        }
+    }
+    for (; v < s.hi; v += kThreads) {
+        float ru[VEC], rz[VEC], rg[VEC];
+        const uint64_t i1 = access_index(g, cbase, v);
+        load_vec<DT, VEC, kHintBwdApplyLoad>(u, i1, ru);
+        load_sign<DT, VEC, kHintBwdApplyLoad, BM>(zs, i1, rz);
+        load_vec<DT, VEC, kHintBwdApplyLoad>(dzdx, i1, rg);
+#pragma unroll
+        for (int k = 0; k < VEC; ++k) rg[k] = dx_of(ru[k], rz[k], rg[k]);
+        store_vec<DT, VEC, kHintBwdApplyStore>(dzdx, i1, rg);
     }
 }
 
@@ -504,8 +487,7 @@ template <int DT, int VEC>
 struct LaunchRecompute {
     static void run(const void* xhat, void* z, const Geom& g, const float* gamma, const float* beta,
                     float slope, hipStream_t st) {
-        recompute_kernel<DT, VEC, unroll<DT, VEC>()><<<grid_of(g), kThreads, 0, st>>>(xhat, z, g, gamma,
-                                                                                   beta, slope);
+        recompute_kernel<DT, VEC><<<grid_of(g), kThreads, 0, st>>>(xhat, z, g, gamma, beta, slope);
     }
 };
 
