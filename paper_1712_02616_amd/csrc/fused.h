@@ -14,8 +14,9 @@ namespace iabn_impl {
 // accesses in registers between the reduction and the apply phase,
 // so those bytes cross HBM once on the way in and once on the way out (the
 // forward reads x and writes z; the backward reads z and dz and writes dx).
-// Accesses beyond R (channels larger than the block's registers) are read
-// again in the apply phase.  Thread t handles accesses t, t + T, t + 2T, ...
+// Accesses beyond R (channels larger than the block's registers) wait in LDS
+// where 1024-thread blocks have room, and are read again in the apply phase
+// otherwise.  Thread t handles accesses t, t + T, t + 2T, ...
 // of its channel, so a wave touches consecutive vectors.  The only
 // synchronisation is the block barrier around the channel's reduction.
 

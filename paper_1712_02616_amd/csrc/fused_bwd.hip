@@ -1,6 +1,7 @@
 // The channel-resident backward: one block per channel holds the stored
-// tensor(s) and dz in registers from the reduction to the apply, so each
-// crosses HBM once in and dx once out.  Formulations as in common.h
+// tensor(s) and dz in registers (and, in 1024-thread blocks, LDS) from the
+// reduction to the apply, so each crosses HBM once in and dx once out (what
+// does not fit is read again).  Formulations as in common.h
 // (InPlace-ABN I and II from z, standard from x and the signs of z,
 // checkpointing from xhat).
 

@@ -1,6 +1,7 @@
 // The channel-resident training forward: one block per channel holds the
-// channel's accesses in registers from the statistics to the apply,
-// so x crosses HBM once in and the outputs once out.  Output modes as in
+// channel's accesses in registers (and, in 1024-thread blocks, LDS) from the
+// statistics to the apply, so x crosses HBM once in and the outputs once out
+// (what does not fit is read again).  Output modes as in
 // common.h (InPlace-ABN, standard, checkpointing).
 
 #include "fused.h"
