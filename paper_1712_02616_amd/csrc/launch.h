@@ -73,8 +73,9 @@ inline size_t fused_lds(int blocks_per_cu) {
 
 // Candidate (T, R) in order of preference (each one has a kernel built in
 // launch_fwd_fused / launch_bwd_fused): the first whose threads hold the
-// whole channel is used; larger channels take the last entry and re-read
-// the remainder.  The backward holds two tensors, so its largest blocks keep
+// whole channel is used; larger channels take the last entry, which keeps
+// part of the remainder in LDS and reads the rest again.  The backward holds
+// two tensors, so its largest blocks keep
 // 11 accesses per thread of each (the most that fits a 1024-thread block's
 // 128 registers per thread in every mode without spilling; 11 instead of 8
 // took the 256-channel layers of the backbone sweep from 41 to 38 us).
