@@ -323,6 +323,7 @@ bool launch_v(const void* u, const void* zs, void* dzdx, const Geom& g, const Fu
     } else if constexpr (BM == kBwdFromZ) {
         IABN_FUSED_CASE_GENERAL(256, 4)
         IABN_FUSED_CASE_GENERAL(256, 8)
+        IABN_FUSED_CASE_GENERAL(512, 4)
         IABN_FUSED_CASE_GENERAL(256, 16)
         IABN_FUSED_CASE_GENERAL(512, 16)
         IABN_FUSED_CASE_GENERAL(1024, 16)

@@ -265,6 +265,7 @@ bool launch_v(void* xz, const Geom& g, const FusedPlan& fp, const FwdParams& prm
     } else if constexpr (FM == kFwdInPlace) {
         IABN_FUSED_CASE_GENERAL(256, 4)
         IABN_FUSED_CASE_GENERAL(256, 8)
+        IABN_FUSED_CASE_GENERAL(512, 4)
         IABN_FUSED_CASE_GENERAL(256, 16)
         IABN_FUSED_CASE_GENERAL(512, 16)
         IABN_FUSED_CASE_GENERAL(1024, 16)

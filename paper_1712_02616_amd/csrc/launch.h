@@ -105,6 +105,11 @@ constexpr FusedPlan kBwdLadder[] = {{256, 4}, {256, 8}, {256, 16}, {512, 16}, {1
 // blocks take the streaming kernels on such shapes).  (One wave per channel
 // for the small channels of 7x7 maps measured no faster than these rungs.)
 constexpr FusedPlan kNarrowLadder[] = {{256, 4}, {256, 8}, {256, 16}, {512, 16}, {1024, 16}};
+// With at most one channel per CU, channels of 1025-2048 narrow accesses take
+// 512-thread blocks instead (2-5% faster on 14x14 and 7x7 fp16 maps with 128
+// to 256 channels; 3-7% slower with 512).
+constexpr FusedPlan kNarrowLadderFew[] = {{256, 4}, {512, 4}, {256, 16}, {512, 16}, {1024, 16}};
+static_assert(sizeof kNarrowLadderFew == sizeof kNarrowLadder, "the narrow ladders have one length");
 
 // elem_bytes: storage size; narrow_ok: whether this entry point has narrow
 // channel-resident kernels.
@@ -113,7 +118,9 @@ inline bool plan_fused(int64_t C, const Geom& g, int elem_bytes, bool backward, 
     if (C < kFusedMinChannels && !fused_few_channels_ok(C, g.vchan, backward)) return false;
     const bool wide = static_cast<int>(g.vec) * elem_bytes == 16;
     if (!wide && !narrow_ok) return false;
-    const FusedPlan* ladder = !wide ? kNarrowLadder : backward ? kBwdLadder : kFwdLadder;
+    const FusedPlan* ladder = !wide ? (C <= kFusedMinChannels ? kNarrowLadderFew : kNarrowLadder)
+                              : backward ? kBwdLadder
+                                         : kFwdLadder;
     const int n = !wide      ? int(sizeof kNarrowLadder / sizeof kNarrowLadder[0])
                   : backward ? int(sizeof kBwdLadder / sizeof kBwdLadder[0])
                              : int(sizeof kFwdLadder / sizeof kFwdLadder[0]);

@@ -113,6 +113,8 @@ EDGE_CASES = [
     Case("narrow2_bigchan_f16", 384, 256, 49, "f16", 37, dz_std=0.1),
     Case("narrow4_rung256_bf16", 64, 300, 98, "bf16", 38, dz_std=0.1),
     Case("narrow4_rung512_f16", 128, 256, 98, "f16", 39, dz_std=0.1),
+    Case("narrow8_few_c200_f16", 32, 200, 196, "f16", 47, dz_std=0.1, gamma_sign=True),
+    Case("narrow2_few_c256_bf16", 32, 256, 49, "bf16", 48, dz_std=0.1),
 ]
 ALL_CASES = CONFIG_CASES + EDGE_CASES
 
