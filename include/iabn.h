@@ -87,6 +87,48 @@ const char *iabn_last_error(void);
  * invalid shape or dtype. */
 size_t iabn_workspace_size(int64_t N, int64_t C, int64_t HW, int dtype);
 
+/* The entry points iabn_plan describes. */
+typedef enum {
+    IABN_OP_FORWARD_TRAIN = 0, /* iabn_forward_train */
+    IABN_OP_BACKWARD = 1,      /* iabn_backward and iabn_backward_ii */
+    IABN_OP_STD_FORWARD = 2,   /* iabn_std_forward_train */
+    IABN_OP_STD_BACKWARD = 3,  /* iabn_std_backward */
+    IABN_OP_CKPT_FORWARD = 4,  /* iabn_ckpt_forward_train */
+    IABN_OP_CKPT_BACKWARD = 5, /* iabn_ckpt_backward */
+    IABN_OP_FORWARD_EVAL = 6,  /* iabn_forward_eval */
+    IABN_OP_CKPT_RECOMPUTE = 7 /* iabn_ckpt_recompute */
+} iabn_op_t;
+
+/* How an entry point runs a shape. */
+typedef struct {
+    int channel_resident; /* 1: one kernel, one block per channel holding the
+                             channel on chip; 0: the streaming kernels (two
+                             passes for the training entry points) */
+    int access_bytes;     /* bytes per vector access: 16, 8, 4, 2, or the
+                             element size */
+    int threads;          /* threads per block */
+    int reg_accesses;     /* channel-resident: accesses per thread held in
+                             registers (per tensor) */
+    int lds_accesses;     /* channel-resident: further accesses per thread
+                             held in LDS (per tensor); any beyond are read
+                             twice */
+    int strips;           /* channel-resident: strip addressing (rows of
+                             whole block-wide strips) */
+    int xcd_order;        /* 1: blocks on each XCD take a contiguous range of
+                             channels (or slices), for rows that do not end
+                             on a 128-byte line */
+    int64_t blocks;       /* blocks per kernel launch */
+} iabn_plan_t;
+
+/* The kernels entry point `op` (an iabn_op_t) runs for this shape and
+ * storage type, with every tensor 16-byte aligned (a tensor that is not can
+ * only make the accesses narrower).  Host only: needs no GPU, launches
+ * nothing.  For callers that schedule around the library, and for tests of
+ * the library's choices.  Validates like the entry point (shape, dtype; a
+ * NULL plan is IABN_ERR_NULL, an unknown op IABN_ERR_PARAM); an empty shape
+ * gives an all-zero plan. */
+int iabn_plan(int op, int dtype, int64_t N, int64_t C, int64_t HW, iabn_plan_t *plan);
+
 /*
  * Training-mode forward, Algorithm 1, in place.
  *   x_z            in: x; out: z = f(gamma * (x - mu)/sqrt(sigma^2 + eps) + beta),

@@ -29,10 +29,22 @@ __all__ = [
     "iabn_workspace_size", "iabn_forward_train", "iabn_forward_eval", "iabn_backward",
     "iabn_forward_stats", "iabn_forward_apply", "iabn_backward_reduce", "iabn_backward_apply",
     "iabn_backward_ii", "iabn_std_forward_train", "iabn_std_backward", "iabn_ckpt_forward_train",
-    "iabn_ckpt_recompute", "iabn_ckpt_backward", "DTYPE_CODES",
+    "iabn_ckpt_recompute", "iabn_ckpt_backward", "iabn_plan", "DTYPE_CODES", "OPS",
 ]
 
 DTYPE_CODES = {torch.float32: 0, torch.float16: 1, torch.bfloat16: 2}
+
+# iabn_op_t: the entry points iabn_plan describes.
+OPS = {"forward_train": 0, "backward": 1, "std_forward": 2, "std_backward": 3,
+       "ckpt_forward": 4, "ckpt_backward": 5, "forward_eval": 6, "ckpt_recompute": 7}
+
+
+class _Plan(ctypes.Structure):
+    """iabn_plan_t."""
+    _fields_ = [("channel_resident", ctypes.c_int), ("access_bytes", ctypes.c_int),
+                ("threads", ctypes.c_int), ("reg_accesses", ctypes.c_int),
+                ("lds_accesses", ctypes.c_int), ("strips", ctypes.c_int),
+                ("xcd_order", ctypes.c_int), ("blocks", ctypes.c_int64)]
 
 _lib = None
 _lib_lock = threading.Lock()
@@ -84,6 +96,7 @@ def declare(lib):
         "iabn_ckpt_forward_train": ([vp, vp, i32, vp, vp, vp, vp, vp, vp, f32, f32, f32, i64, i64, i64, vp, sz, vp], i32),
         "iabn_ckpt_recompute": ([vp, vp, i32, vp, vp, f32, i64, i64, i64, vp], i32),
         "iabn_ckpt_backward": ([vp, vp, i32, vp, vp, vp, vp, vp, f32, f32, i64, i64, i64, vp, sz, vp], i32),
+        "iabn_plan": ([i32, i32, i64, i64, i64, ctypes.POINTER(_Plan)], i32),
     }
     for name, (args, res) in sig.items():
         fn = getattr(lib, name)
@@ -164,6 +177,18 @@ def iabn_workspace_size(N: int, C: int, HW: int, dtype) -> int:
     """Workspace bytes for a shape; ``dtype`` is a torch dtype or a dtype code."""
     code = DTYPE_CODES[dtype] if isinstance(dtype, torch.dtype) else int(dtype)
     return int(load().iabn_workspace_size(int(N), int(C), int(HW), code))
+
+
+def iabn_plan(op, dtype, N: int, C: int, HW: int) -> dict:
+    """How entry point ``op`` (a name of ``OPS`` or an iabn_op_t code) runs a
+    shape with aligned tensors: the fields of iabn_plan_t as a dict.  Host
+    only."""
+    code = DTYPE_CODES[dtype] if isinstance(dtype, torch.dtype) else int(dtype)
+    opc = OPS[op] if isinstance(op, str) else int(op)
+    plan = _Plan()
+    rc = load().iabn_plan(opc, code, int(N), int(C), int(HW), ctypes.byref(plan))
+    _check("iabn_plan", rc)
+    return {name: int(getattr(plan, name)) for name, _ in _Plan._fields_}
 
 
 def iabn_forward_train(x_z, gamma, beta, running_mean, running_var, save_mean, save_var,

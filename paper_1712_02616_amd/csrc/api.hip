@@ -266,6 +266,42 @@ size_t iabn_workspace_size(int64_t N, int64_t C, int64_t HW, int dtype) {
     return workspace_bytes_for(N, C, HW);
 }
 
+int iabn_plan(int op, int dtype, int64_t N, int64_t C, int64_t HW, iabn_plan_t* plan) {
+    if (plan == nullptr) return fail(IABN_ERR_NULL, "plan is NULL");
+    if (op < IABN_OP_FORWARD_TRAIN || op > IABN_OP_CKPT_RECOMPUTE)
+        return fail(IABN_ERR_PARAM, "unknown op %d", op);
+    const bool train = op != IABN_OP_FORWARD_EVAL && op != IABN_OP_CKPT_RECOMPUTE;
+    int rc = validate_common(dtype, N, C, HW, train);
+    if (rc) return rc;
+    memset(plan, 0, sizeof *plan);
+    if (empty(N, C, HW)) return ok();
+    // The same choices as the entry points make, on aligned tensors.
+    const int vec = access_vec(HW, dtype, nullptr, nullptr, nullptr);
+    const Geom g = make_geom(N, C, HW, dtype, vec);
+    const int eb = elem_bytes(dtype);
+    const bool backward =
+        op == IABN_OP_BACKWARD || op == IABN_OP_STD_BACKWARD || op == IABN_OP_CKPT_BACKWARD;
+    const bool narrow_ok = op == IABN_OP_FORWARD_TRAIN || op == IABN_OP_BACKWARD;
+    plan->access_bytes = vec * eb;
+    plan->xcd_order = static_cast<int>(g.xcd_order);
+    FusedPlan fp;
+    if (train && plan_fused(C, g, eb, backward, narrow_ok, &fp)) {
+        const int64_t past = static_cast<int64_t>(g.vchan) - static_cast<int64_t>(fp.T) * fp.R;
+        const int64_t past_per_thread = past > 0 ? (past + fp.T - 1) / fp.T : 0;
+        const int64_t lds = fused_lds_accesses(fp.T, backward, op == IABN_OP_STD_BACKWARD);
+        plan->channel_resident = 1;
+        plan->threads = fp.T;
+        plan->reg_accesses = fp.R;
+        plan->lds_accesses = static_cast<int>(past_per_thread < lds ? past_per_thread : lds);
+        plan->strips = fused_strips(g, fp, vec * eb == 16) ? 1 : 0;
+        plan->blocks = C;
+    } else {
+        plan->threads = kThreads;
+        plan->blocks = C * static_cast<int64_t>(g.P);
+    }
+    return ok();
+}
+
 int iabn_forward_stats(const void* x, int dtype, int64_t N, int64_t C, int64_t HW,
                        void* workspace, size_t workspace_bytes, void* stream) {
     int rc = validate_common(dtype, N, C, HW, true);

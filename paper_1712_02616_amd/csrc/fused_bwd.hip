@@ -45,7 +45,7 @@ __device__ __forceinline__ void bwd_fused_channel(const void* __restrict__ u,
     // whose registers hold 11 per tensor) wait in LDS from the reduction to
     // the apply phase instead of being read again; each thread reads back
     // only its own slots.  kBwdFromXZ keeps its third tensor (z) there too.
-    constexpr int S = T == 1024 ? (XZ ? kBwdLdsAccessesXZ : kBwdLdsAccesses) : 0;
+    constexpr int S = fused_lds_accesses(T, true, XZ);
     __shared__ raw_t<DT, VEC> lu[S > 0 ? S : 1][T], lg[S > 0 ? S : 1][T];
     __shared__ raw_t<DT, VEC> lz[XZ && S > 0 ? S : 1][T];
     uint32_t negm[NW];
@@ -296,7 +296,7 @@ __global__ __launch_bounds__(T) void bwd_fused_kernel(const void* __restrict__ u
 
 #define IABN_FUSED_CASE(TT, RR)                                                              \
     if (fp.T == TT && fp.R == RR) {                                                           \
-        if (kUseStrips && g.vrow % TT == 0 && g.vchan / TT >= RR)                             \
+        if (fused_strips(g, fp, true))                                                        \
             bwd_fused_kernel<DT, V, TT, RR, true, BM><<<grid, TT, lds, st>>>(u, zs, dzdx, g, prm);  \
         else                                                                                  \
             bwd_fused_kernel<DT, V, TT, RR, false, BM><<<grid, TT, lds, st>>>(u, zs, dzdx, g, prm); \

@@ -115,7 +115,7 @@ __device__ __forceinline__ void fwd_fused_channel(void* __restrict__ xz, const G
     // The first S accesses per thread past the registers (1024-thread
     // blocks) wait in LDS for the apply phase instead of being read again;
     // each thread reads back only its own slots.
-    constexpr int S = T == 1024 ? kFwdLdsAccesses : 0;
+    constexpr int S = fused_lds_accesses(T, false, false);
     __shared__ raw_t<DT, VEC> lx[S > 0 ? S : 1][T];
     StripPos sp = strip_begin(g, c);
 #pragma unroll
@@ -238,7 +238,7 @@ __global__ __launch_bounds__(T) void fwd_fused_kernel(void* __restrict__ xz, Geo
 
 #define IABN_FUSED_CASE(TT, RR)                                                              \
     if (fp.T == TT && fp.R == RR) {                                                           \
-        if (kUseStrips && g.vrow % TT == 0 && g.vchan / TT >= RR)                             \
+        if (fused_strips(g, fp, true))                                                        \
             fwd_fused_kernel<DT, V, TT, RR, true, FM><<<grid, TT, lds, st>>>(xz, g, prm);     \
         else                                                                                  \
             fwd_fused_kernel<DT, V, TT, RR, false, FM><<<grid, TT, lds, st>>>(xz, g, prm);    \

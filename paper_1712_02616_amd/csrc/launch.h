@@ -95,6 +95,12 @@ constexpr int kFwdLdsAccesses = 9;
 constexpr int kBwdLdsAccesses = 4;
 constexpr int kBwdLdsAccessesXZ = 3;
 
+// LDS slots per thread of a channel-resident kernel with T threads (xz: the
+// standard block's backward, which keeps three tensors).
+constexpr int fused_lds_accesses(int T, bool backward, bool xz) {
+    return T != 1024 ? 0 : !backward ? kFwdLdsAccesses : xz ? kBwdLdsAccessesXZ : kBwdLdsAccesses;
+}
+
 constexpr FusedPlan kFwdLadder[] = {{256, 4}, {256, 8}, {256, 16}, {512, 16}, {1024, 16}};
 constexpr FusedPlan kBwdLadder[] = {{256, 4}, {256, 8}, {256, 16}, {512, 16}, {1024, 11}};
 
@@ -132,6 +138,13 @@ inline bool plan_fused(int64_t C, const Geom& g, int elem_bytes, bool backward, 
         }
     }
     return false;
+}
+
+// Strip addressing: 16-byte accesses whose rows hold whole T-wide strips,
+// at least R of them per channel.
+inline bool fused_strips(const Geom& g, const FusedPlan& fp, bool wide) {
+    return wide && kUseStrips && g.vrow % static_cast<uint32_t>(fp.T) == 0 &&
+           g.vchan / static_cast<uint32_t>(fp.T) >= static_cast<uint32_t>(fp.R);
 }
 
 // False if no kernel is built for the plan's (T, R) (a planning bug).

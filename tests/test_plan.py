@@ -1,0 +1,132 @@
+"""The library's choice of kernels per shape, through iabn_plan (host only,
+no GPU): which path runs, the block and register depth of the
+channel-resident kernels, what waits in LDS, strip addressing, access
+width and the XCD order.  These are the decisions the measurements behind
+the kernels settled; a change to any of them shows up here first.
+"""
+
+import pytest
+import torch
+
+import paper_1712_02616_amd as iabn
+
+F32, F16, BF16 = torch.float32, torch.float16, torch.bfloat16
+
+
+def plan(op, dtype, N, C, HW):
+    return iabn.iabn_plan(op, dtype, N, C, HW)
+
+
+def fused(p, T, R, lds=0, strips=None, access=16, xcd=0, blocks=None):
+    assert p["channel_resident"] == 1, p
+    assert (p["threads"], p["reg_accesses"], p["lds_accesses"]) == (T, R, lds), p
+    assert p["access_bytes"] == access and p["xcd_order"] == xcd, p
+    if strips is not None:
+        assert p["strips"] == strips, p
+    if blocks is not None:
+        assert p["blocks"] == blocks, p
+
+
+def streaming(p, access=16, xcd=0, blocks=None):
+    assert p["channel_resident"] == 0 and p["threads"] == 256, p
+    assert p["reg_accesses"] == p["lds_accesses"] == p["strips"] == 0, p
+    assert p["access_bytes"] == access and p["xcd_order"] == xcd, p
+    if blocks is not None:
+        assert p["blocks"] == blocks, p
+
+
+@pytest.mark.parametrize("op", ["forward_train", "backward"])
+def test_backbone_sweep_layers(op):
+    """The four layer shapes of the benchmark's sweep (fp16, N = 8)."""
+    bwd = op == "backward"
+    # C = 256 at 128x128: 16 strips of 1024 accesses; the backward keeps 11 in
+    # registers and 4 in LDS.
+    fused(plan(op, F16, 8, 256, 128 * 128), 1024, 11 if bwd else 16, lds=4 if bwd else 0,
+          strips=1, blocks=256)
+    for C in (512, 1024, 2048):
+        fused(plan(op, F16, 8, C, 64 * 64), 256, 16, strips=1, blocks=C)
+
+
+def test_parity_workloads():
+    # ResNet layer, fp32: 25088 accesses per channel, the last rung with LDS.
+    fused(plan("forward_train", F32, 32, 256, 56 * 56), 1024, 16, lds=9, strips=0)
+    fused(plan("backward", F32, 32, 256, 56 * 56), 1024, 11, lds=4, strips=0)
+    # Segmentation crop: 18432 accesses, two strips past the forward's registers.
+    fused(plan("forward_train", F16, 4, 256, 192 * 192), 1024, 16, lds=2, strips=0)
+    # Wide layer: 1568 accesses per channel, rows of 1568 bytes (not whole lines).
+    fused(plan("forward_train", BF16, 16, 2048, 28 * 28), 256, 8, strips=0, xcd=1, blocks=2048)
+    # Tiny layer: streaming.
+    streaming(plan("forward_train", F32, 2, 16, 8 * 8))
+
+
+def test_few_channel_rule():
+    # Forward from 64 channels, backward from 96, while a channel fits.
+    fused(plan("forward_train", F16, 32, 64, 56 * 56), 1024, 16)
+    streaming(plan("backward", F16, 32, 64, 56 * 56))
+    fused(plan("backward", F16, 32, 96, 56 * 56), 1024, 11, lds=2)
+    streaming(plan("forward_train", F16, 32, 63, 56 * 56))
+    # Up to 16K accesses below 128 channels, 32K from 128.
+    streaming(plan("forward_train", F16, 8, 96, 256 * 256 // 2))
+    fused(plan("forward_train", F32, 32, 128, 56 * 56), 1024, 16, lds=9)
+    streaming(plan("forward_train", F16, 8, 128, 36864))
+    # A stem-like layer (64 channels of 256x256) stays on the streaming kernels.
+    streaming(plan("forward_train", F16, 8, 64, 256 * 256), blocks=64 * 8)
+    streaming(plan("backward", F16, 8, 64, 256 * 256), blocks=64 * 8)
+
+
+def test_rungs():
+    # 1025-2048 accesses: (256, 8) on the 16-byte path.
+    fused(plan("forward_train", F16, 8, 300, 2048), 256, 8, strips=1)
+    fused(plan("backward", F16, 8, 300, 2048), 256, 8, strips=1)
+    # Narrow rows with at most one channel per CU: (512, 4); with more: (256, 8).
+    fused(plan("backward", F16, 32, 200, 14 * 14), 512, 4, access=8, xcd=1)
+    fused(plan("backward", F16, 32, 1024, 14 * 14), 256, 8, access=8, xcd=1)
+    fused(plan("forward_train", F16, 32, 2048, 7 * 7), 256, 8, access=2, xcd=1)
+
+
+def test_comparison_blocks():
+    # The standard block keeps three tensors in the backward: 3 per tensor in LDS.
+    fused(plan("std_backward", F16, 8, 256, 128 * 128), 1024, 11, lds=3, strips=1)
+    fused(plan("ckpt_backward", F16, 8, 256, 128 * 128), 1024, 11, lds=4, strips=1)
+    fused(plan("std_forward", F16, 8, 1024, 64 * 64), 256, 16, strips=1)
+    fused(plan("ckpt_forward", F16, 8, 1024, 64 * 64), 256, 16, strips=1)
+    # Narrow rows: the comparison blocks take the streaming kernels.
+    streaming(plan("std_forward", F16, 32, 2048, 7 * 7), access=2, xcd=1)
+    streaming(plan("ckpt_backward", F16, 32, 2048, 7 * 7), access=2, xcd=1)
+
+
+def test_always_streaming_entry_points():
+    for op in ("forward_eval", "ckpt_recompute"):
+        streaming(plan(op, F16, 8, 1024, 64 * 64), blocks=1024)
+        streaming(plan(op, F16, 32, 2048, 7 * 7), access=2, xcd=1)
+        # Inference accepts a single value per channel (4-byte rows: XCD order).
+        streaming(plan(op, F32, 1, 4, 1), access=4, xcd=1)
+
+
+def test_access_width_and_xcd_order():
+    # The widest access that divides a row; XCD order exactly when a row's
+    # bytes are not a multiple of 128.
+    assert plan("forward_eval", F16, 4, 8, 64)["access_bytes"] == 16     # 128-byte rows
+    assert plan("forward_eval", F16, 4, 8, 64)["xcd_order"] == 0
+    assert plan("forward_eval", F16, 4, 8, 68)["access_bytes"] == 8      # 136-byte rows
+    assert plan("forward_eval", F16, 4, 8, 68)["xcd_order"] == 1
+    assert plan("forward_eval", F32, 4, 8, 3)["access_bytes"] == 4
+    assert plan("forward_eval", BF16, 4, 8, 3)["access_bytes"] == 2
+    assert plan("forward_eval", F32, 4, 8, 96)["xcd_order"] == 0        # 384-byte rows
+
+
+def test_empty_and_invalid():
+    for shape in ((8, 0, 64), (0, 8, 64)):
+        assert all(v == 0 for v in plan("forward_eval", F16, *shape).values())
+    assert all(v == 0 for v in plan("forward_train", F16, 8, 0, 64).values())
+    with pytest.raises(iabn.IabnError) as e:
+        plan("forward_train", F16, 1, 4, 1)  # one value per channel in training
+    assert e.value.status == 2
+    with pytest.raises(iabn.IabnError) as e:
+        iabn.iabn_plan(8, F16, 2, 4, 4)
+    assert e.value.status == 3
+    with pytest.raises(iabn.IabnError) as e:
+        iabn.iabn_plan(0, 7, 2, 4, 4)
+    assert e.value.status == 4
+    lib = iabn.load()
+    assert lib.iabn_plan(0, 1, 2, 4, 4, None) == 1
