@@ -29,6 +29,18 @@ known size), read from the committed profile summary and reported only
 while the kernel sources are unchanged since.  ``cpu_baseline`` is the
 double-precision oracle on the host's cores over whole layers of the same
 workload, bounded in time.
+
+``ceiling_gbps`` is what this part sustains over the same buffers for each
+access mix of the kernels (read only; one read and one in-place write, the
+forward's; two reads and one in-place write, the backward's), measured by
+the bandwidth probes of ``libiabn_probe.so`` (16-byte non-temporal accesses,
+no arithmetic; streaming grid-stride loops over several grid sizes, and the
+channel-resident load / barrier / store pattern), the best rate per mix.
+``activation_memory`` is measured: each block's training forward runs over
+the layers with the buffers it keeps for the backward allocated through
+torch's allocator (InPlace-ABN: z over x; the standard block: x and a new z;
+the checkpointing: xhat over x, z transient), and the peak of allocated
+device memory above the starting point is recorded.
 """
 
 from __future__ import annotations
@@ -70,6 +82,8 @@ def parse():
     ap.add_argument("--no-arms", action="store_true",
                     help="skip timing the other blocks of Sec. 3.2 (InPlace-ABN II, standard, "
                          "checkpointing) on the same workload")
+    ap.add_argument("--no-probes", action="store_true",
+                    help="skip the bandwidth-ceiling probes and the activation-memory measurement")
     ap.add_argument("--phase-kernels", action="store_true",
                     help="also time the phase entry points (the streaming kernels), one by one")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -144,6 +158,122 @@ def time_phases(lib, layers, refresh, check, stream, steps, b):
             for name in tot_ms}
 
 
+# Bandwidth probes (bench_probe.hip): mix code, tensors read, tensors written
+# (per element, units of the storage size b), whether the grid is chosen.
+PROBE_MIXES = {"read": (0, 2, 0, True), "rw_1r1w": (1, 1, 1, True), "rmw_2r1w": (2, 2, 1, True),
+               "resident_rw_1r1w": (3, 1, 1, False), "resident_rmw_2r1w": (4, 2, 1, False)}
+PROBE_GRIDS = (2048, 4096, 8192, 16384, 32768)
+
+
+def load_probe():
+    """libiabn_probe.so (the benchmark's bandwidth probes), built by build()."""
+    from paper_1712_02616_amd import build as hip_build
+    if not os.path.exists(hip_build.PROBE_LIB):
+        hip_build.build_probe()
+    lib = ctypes.CDLL(hip_build.PROBE_LIB)
+    lib.iabn_probe_launch.argtypes = [ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p,
+                                      ctypes.c_size_t, ctypes.c_int, ctypes.c_uint,
+                                      ctypes.c_void_p, ctypes.c_void_p]
+    lib.iabn_probe_launch.restype = ctypes.c_int
+    return lib
+
+
+def time_probes(layers, stream, reps, b):
+    """Attainable HBM rate of each access mix over the layers' own x and dz
+    buffers (the same working set, in the same order as the passes), chained
+    layer after layer and timed with HIP events on the stream; for the
+    streaming mixes, the best of several grid sizes."""
+    import torch
+    probe = load_probe()
+    sink = torch.zeros(64, dtype=torch.int32, device=layers[0].x.device)
+    sp = ctypes.c_void_p(stream.cuda_stream)
+    out = {}
+    for name, (mix, nread, nwrite, gridded) in PROBE_MIXES.items():
+        best = None
+        for grid in (PROBE_GRIDS if gridded else (1,)):
+            def one_pass():
+                for L in layers:
+                    rc = probe.iabn_probe_launch(mix, L.x.data_ptr(), L.dz.data_ptr(),
+                                                 L.E * b, grid, 0, sink.data_ptr(), sp)
+                    if rc != 0:
+                        raise RuntimeError("iabn_probe_launch(%s) failed: %d" % (name, rc))
+            one_pass()
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for _ in range(reps):
+                one_pass()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            ms = e0.elapsed_time(e1)
+            nbytes = (nread + nwrite) * sum(L.E for L in layers) * b * reps
+            gbps = nbytes / (ms * 1e-3) / 1e9
+            if best is None or gbps > best[0]:
+                best = (gbps, grid if gridded else None, ms / (reps * len(layers)) * 1e3)
+        out[name] = {"gbps": round(best[0], 1), "grid": best[1], "avg_us_per_layer": round(best[2], 3),
+                     "reads_per_elem": nread, "writes_per_elem": nwrite}
+    return out
+
+
+def measure_activation_memory(lib, layers, check, dev, code, w, wsp, ws_bytes, sp):
+    """Peak device memory above the starting point while each block's
+    training forward runs over the layers, keeping what that block keeps for
+    its backward; every kept buffer is a fresh allocation through torch's
+    allocator.  InPlace-ABN: the layer's input x (as a convolution would
+    deliver it) becomes z in place.  Standard: x is kept and z is a second
+    buffer.  Checkpointing: x becomes xhat in place, z is written to a buffer
+    that is released after the layer (the next layer's input would be made
+    from it).  Also the change of the device's free memory (hipMemGetInfo) with
+    torch's cache emptied first."""
+    import torch
+    p = lambda t: ctypes.c_void_p(t.data_ptr())  # noqa: E731
+
+    def forward_keeping(block):
+        """The block's forward over every layer; returns what it keeps."""
+        kept = []
+        for L in layers:
+            N, C, HW = L.shape
+            x = torch.empty_like(L.x0)
+            x.copy_(L.x0)
+            stats = (p(L.gamma), p(L.beta), p(L.rm), p(L.rv), p(L.sm), p(L.sv), w.eps, w.momentum,
+                     w.slope, N, C, HW, wsp, ws_bytes, sp)
+            if block == "inplace_abn":
+                check(lib.iabn_forward_train(p(x), code, *stats), block)
+                kept.append(x)
+            elif block == "standard":
+                z = torch.empty_like(x)
+                check(lib.iabn_std_forward_train(p(x), p(z), code, *stats), block)
+                kept += [x, z]
+            else:
+                z = torch.empty_like(x)
+                check(lib.iabn_ckpt_forward_train(p(x), p(z), code, *stats), block)
+                kept.append(x)
+                del z  # the stream orders its reuse after the forward
+        return kept
+
+    out = {}
+    for block in ("inplace_abn", "standard", "checkpointing"):
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+        torch.cuda.reset_peak_memory_stats(dev)
+        base = torch.cuda.memory_allocated(dev)
+        free0 = torch.cuda.mem_get_info(dev)[0]
+        kept = forward_keeping(block)
+        torch.cuda.synchronize()
+        peak = torch.cuda.max_memory_allocated(dev) - base
+        held = torch.cuda.memory_allocated(dev) - base
+        free_delta = free0 - torch.cuda.mem_get_info(dev)[0]
+        out[block] = {"peak_allocated_bytes": int(peak), "kept_bytes": int(held),
+                      "device_free_delta_bytes": int(free_delta)}
+        del kept
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    for block in ("standard", "checkpointing"):
+        out["inplace_abn_peak_vs_" + block] = round(
+            out["inplace_abn"]["peak_allocated_bytes"] / out[block]["peak_allocated_bytes"], 4)
+    return out
+
+
 class Layer:
     pass
 
@@ -168,8 +298,8 @@ def time_arms(lib, layers, refresh, check, stream, args, E_total, b, iabn_kernel
     signs of z) and the proposed checkpointing (keeps xhat; the backward
     recomputes z from xhat, then runs from xhat).  Per block: ms per step,
     average forward / backward time per layer, algorithmic bytes per element
-    (units of the storage size b) and the activation bytes kept for the
-    backward."""
+    (units of the storage size b); the activation memory each block keeps is
+    measured by measure_activation_memory."""
     import torch
     p = lambda t: ctypes.c_void_p(t.data_ptr())  # noqa: E731
     zmax = max(L.E for L in layers)
@@ -189,15 +319,15 @@ def time_arms(lib, layers, refresh, check, stream, args, E_total, b, iabn_kernel
                     w.eps, w.slope, N, C, HW, wsp, ws_bytes, sp)
     blocks = {
         "inplace_abn_ii": ([(lib.iabn_forward_train, "fwd")],
-                           [(lib.iabn_backward_ii, "bwd")], 2, 3, 1),
+                           [(lib.iabn_backward_ii, "bwd")], 2, 3),
         "standard": ([(lib.iabn_std_forward_train, "std_fwd")],
-                     [(lib.iabn_std_backward, "std_bwd")], 2, 4, 2),
+                     [(lib.iabn_std_backward, "std_bwd")], 2, 4),
         "checkpointing": ([(lib.iabn_ckpt_forward_train, "ck_fwd")],
                           [(lib.iabn_ckpt_recompute, "ck_rec"), (lib.iabn_ckpt_backward, "ck_bwd")],
-                          3, 5, 1),
+                          3, 5),
     }
     out = {}
-    for name, (fcalls, bcalls, fb, bb, kept) in blocks.items():
+    for name, (fcalls, bcalls, fb, bb) in blocks.items():
         def fwd_pass():
             for L in layers:
                 for fn, attr in fcalls:
@@ -231,12 +361,10 @@ def time_arms(lib, layers, refresh, check, stream, args, E_total, b, iabn_kernel
                      "forward_avg_us": round(fwd_ms / n * 1e3, 3),
                      "backward_avg_us": round(bwd_ms / n * 1e3, 3),
                      "alg_bytes_per_elem_b": {"forward": fb, "backward": bb},
-                     "alg_gbps": round((fb + bb) * E_total * b * args.steps / ((fwd_ms + bwd_ms) * 1e-3) / 1e9, 1),
-                     "stored_activation_bytes": kept * E_total * b}
+                     "alg_gbps": round((fb + bb) * E_total * b * args.steps / ((fwd_ms + bwd_ms) * 1e-3) / 1e9, 1)}
     iabn_us = (iabn_kernels["iabn_forward_train"]["avg_us"] + iabn_kernels["iabn_backward"]["avg_us"])
     std_us = out["standard"]["forward_avg_us"] + out["standard"]["backward_avg_us"]
     out["inplace_abn_time_vs_standard"] = round(iabn_us / std_us - 1.0, 4)
-    out["inplace_abn_memory_vs_standard"] = 0.5
     for L in layers:
         del L.zs
     return out
@@ -433,6 +561,22 @@ def measure(lib, args):
                 "iabn_backward_frac": round(kernels["iabn_backward"]["achieved_gbps"] / copy_gbps, 4)}
     log("copy reference: %.1f GB/s" % copy_gbps)
 
+    # ---------------------------------------------------------------- bandwidth ceilings
+    # The probes over the same x and dz buffers (they leave the data as they
+    # found it), and each entry point's rate against the ceiling of its mix.
+    ceiling = None
+    if not args.no_probes:
+        ceiling = time_probes(layers, stream, max(2, args.steps // 2), b)
+        log("bandwidth ceilings: " + json.dumps(ceiling))
+        mixes = {"iabn_forward_train": ("1R:1W", ("rw_1r1w", "resident_rw_1r1w")),
+                 "iabn_backward": ("2R:1W", ("rmw_2r1w", "resident_rmw_2r1w"))}
+        for name, (mix, probes) in mixes.items():
+            best = max(probes, key=lambda q: ceiling[q]["gbps"])
+            kernels[name]["ceiling"] = {"mix": mix, "probe": best, "gbps": ceiling[best]["gbps"],
+                                        "frac": round(kernels[name]["achieved_gbps"] /
+                                                      ceiling[best]["gbps"], 4)}
+        roofline["ceiling"] = kernels[dom]["ceiling"]
+
     # ---------------------------------------------------------------- inference forward
     # The inference forward (running statistics, in place) over the same
     # layers: one read and one write per element.
@@ -462,6 +606,12 @@ def measure(lib, args):
         arms = time_arms(lib, layers, refresh, check, stream, args, E_total, b, kernels, dev, sp,
                          code, w, wsp, ws_bytes)
         log("blocks: " + json.dumps(arms))
+
+    # ---------------------------------------------------------------- activation memory
+    memory = None
+    if not args.no_probes:
+        memory = measure_activation_memory(lib, layers, check, dev, code, w, wsp, ws_bytes, sp)
+        log("activation memory: " + json.dumps(memory))
 
     # ---------------------------------------------------------------- phase kernels
     phase_kernels = None
@@ -545,16 +695,15 @@ def measure(lib, args):
                 "two_pass_schedule_equivalent_gbps": round(sched_bytes / (ms_per_step * 1e-3) / 1e9, 1)},
         "event_ms_per_step": round(ev_ms_per_step, 4),
         "outputs_finite": finite,
-        # What the forward leaves for the backward: InPlace-ABN only the z
-        # buffers (the x buffers, overwritten), the standard block x and z.
-        # One workspace serves every layer and call.
-        "activation_memory": {"iabn_stored_bytes": sum(L.x.untyped_storage().nbytes() for L in layers),
-                              "store_x_baseline_bytes": 2 * E_total * b,
-                              "workspace_bytes": ws_bytes},
+        # Measured (see measure_activation_memory); one workspace serves
+        # every layer and call.
+        "activation_memory": None if memory is None else dict(memory, workspace_bytes=ws_bytes),
         "kernels": kernels,
         "blocks": arms,
         "phase_kernels": phase_kernels,
         "roofline": roofline,
+        "ceiling_gbps": None if ceiling is None else {k: v["gbps"] for k, v in ceiling.items()},
+        "ceiling_probes": ceiling,
         "copy_reference": copy_ref,
         "cpu_baseline": cpu,
     }

@@ -1,7 +1,9 @@
 """Compile libiabn.so (the HIP kernels and the C ABI) for gfx950 with hipcc.
 
 Each translation unit of ``csrc/`` compiles to an object file in parallel,
-then one link makes the shared library.
+then one link makes the shared library.  ``build_probe`` compiles the
+benchmark's bandwidth probes (``bench_probe.hip``) into a library of their
+own, ``libiabn_probe.so``; libiabn does not contain or use them.
 """
 
 from __future__ import annotations
@@ -18,6 +20,8 @@ CSRC = os.path.join(HERE, "csrc")
 SOURCES = sorted(glob.glob(os.path.join(CSRC, "*.hip")))
 HEADERS = sorted(glob.glob(os.path.join(CSRC, "*.h"))) + [os.path.join(ROOT, "include", "iabn.h")]
 LIB = os.path.join(HERE, "libiabn.so")
+PROBE_SRC = os.path.join(HERE, "bench_probe.hip")
+PROBE_LIB = os.path.join(HERE, "libiabn_probe.so")
 ARCH = "gfx950"
 
 FLAGS = ["--offload-arch=" + ARCH, "-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-function",
@@ -65,9 +69,21 @@ def build(verbose: bool = False) -> str:
     return LIB
 
 
+def build_probe() -> str:
+    """Always recompiles libiabn_probe.so (the benchmark's bandwidth probes)."""
+    out = PROBE_LIB + ".tmp%d" % os.getpid()
+    cmd = [hipcc()] + FLAGS + ["-shared", "-o", out, PROBE_SRC]
+    res = subprocess.run(cmd, capture_output=True, text=True)
+    if res.returncode != 0:
+        raise RuntimeError("hipcc failed (%d):\n%s\n%s" % (res.returncode, " ".join(cmd), res.stderr))
+    os.replace(out, PROBE_LIB)
+    return PROBE_LIB
+
+
 def is_built() -> bool:
     return os.path.exists(LIB)
 
 
 if __name__ == "__main__":
     print(build(verbose=True))
+    print(build_probe())

@@ -4,6 +4,7 @@ measured on."""
 
 from __future__ import annotations
 
+import ctypes
 import os
 import subprocess
 import sys
@@ -49,3 +50,17 @@ def test_traffic_withheld_for_other_sources(tmp_path, monkeypatch):
 def test_source_digest_covers_kernels_and_header():
     d = bench.kernel_source_digest()
     assert len(d) == 64 and d == bench.kernel_source_digest()
+
+
+def test_probe_library_validates_before_launching():
+    """The bandwidth probes' C entry point rejects bad arguments on the host
+    (no launch, so this runs without a GPU)."""
+    probe = bench.load_probe()
+    a = ctypes.c_void_p(1 << 20)
+    assert probe.iabn_probe_launch(0, a, a, 0, 1024, 0, a, None) == 1      # no bytes
+    assert probe.iabn_probe_launch(2, a, a, 24, 1024, 0, a, None) == 1     # not a multiple of 16
+    assert probe.iabn_probe_launch(9, a, a, 4096, 1024, 0, a, None) == 1   # unknown mix
+    assert probe.iabn_probe_launch(2, a, None, 4096, 1024, 0, a, None) == 1  # the mix needs b
+    assert probe.iabn_probe_launch(1, ctypes.c_void_p((1 << 20) + 8), None, 4096, 1024, 0, None,
+                                   None) == 1                              # misaligned
+    assert probe.iabn_probe_launch(1, a, None, 4096, 0, 0, None, None) == 1  # no blocks
