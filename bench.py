@@ -77,6 +77,9 @@ def parse():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", type=int, default=5, help="workload index (1-5)")
+    ap.add_argument("--shape", default=None, metavar="N,C,H,W,DTYPE",
+                    help="instead of --config: one layer of this shape (dtype f32, f16 or bf16) "
+                         "with the ResNet layer's value distributions")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="time budget of the oracle baseline (0 disables it)")
     ap.add_argument("--no-arms", action="store_true",
@@ -406,7 +409,12 @@ def measure(lib, args):
 
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    w = workloads.WORKLOADS[args.config]
+    if getattr(args, "shape", None):
+        n, c, h, wd, dt = args.shape.split(",")
+        w = workloads.single_layer(int(n), int(c), int(h), int(wd), dt)
+        args.config = 0
+    else:
+        w = workloads.WORKLOADS[args.config]
     tdt = {"f32": torch.float32, "f16": torch.float16, "bf16": torch.bfloat16}[w.dtype]
     code = iabn.DTYPE_CODES[tdt]
     b = workloads.ELEM_BYTES[w.dtype]

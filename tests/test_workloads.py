@@ -1,6 +1,7 @@
 """The seeded input generator: storage rounding and reproducibility (CPU only)."""
 
 import numpy as np
+import pytest
 import torch
 
 import workloads
@@ -54,3 +55,13 @@ def test_workload_table():
     assert w[5].elements == 1140850688
     assert len(w[5].layers) == 33
     assert [w[k].dtype for k in range(1, 6)] == ["f32", "f32", "f16", "bf16", "f16"]
+
+
+def test_single_layer_workload():
+    w = workloads.single_layer(8, 64, 256, 256, "f16")
+    assert w.layers == ((8, 64, 65536),) and w.dtype == "f16" and w.seed == workloads.BASE_SEED
+    assert w.dz_std == 0.1 and w.name == "layer_8x64x256x256_f16"
+    with pytest.raises(ValueError):
+        workloads.single_layer(8, 64, 0, 256, "f16")
+    with pytest.raises(ValueError):
+        workloads.single_layer(8, 64, 16, 16, "f64")

@@ -82,6 +82,18 @@ WORKLOADS = {
 }
 
 
+def single_layer(N: int, C: int, H: int, W: int, dtype: str) -> Workload:
+    """A one-layer workload of any shape with the ResNet layer's value
+    distributions (dz ~ N(0, 1e-2)) and seed 1712; for measuring layer
+    shapes outside the five workloads above."""
+    if dtype not in DTYPES:
+        raise ValueError("unknown dtype %r" % dtype)
+    if min(N, C, H, W) < 1:
+        raise ValueError("every size must be positive")
+    return Workload(0, "layer_%dx%dx%dx%d_%s" % (N, C, H, W, dtype), dtype, ((N, C, H * W),),
+                    dz_std=0.1)
+
+
 def f64_to_storage(a: np.ndarray, dtype: str) -> np.ndarray:
     """Round float64 values to the storage format (RNE).
 
