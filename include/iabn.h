@@ -43,8 +43,9 @@
  *    the order of the sums, not the result beyond rounding).
  *  - Results are deterministic: the same inputs on the same device give
  *    bit-identical outputs (all reductions combine in a fixed order).
- *  - The library keeps no device state between calls: calls on different
- *    streams may run concurrently when they share no output or workspace.
+ *  - The library keeps no device state between calls (except the scratch
+ *    of iabn_forward_train_noalloc): calls on different streams may run
+ *    concurrently when they share no output or workspace.
  */
 #ifndef IABN_H
 #define IABN_H
@@ -154,6 +155,25 @@ int iabn_forward_train(void *x_z, int dtype, const float *gamma, const float *be
                        float *save_var, float eps, float momentum, float slope, int64_t N,
                        int64_t C, int64_t HW, void *workspace, size_t workspace_bytes,
                        void *stream);
+
+/*
+ * iabn_forward_train without a workspace, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation).  Same arguments, results and
+ * validation as iabn_forward_train; the partial results that the streaming
+ * kernels keep between their two passes go to a static scratch array of
+ * 128 KiB that the library holds on each device (every shape this forward
+ * runs on the streaming kernels needs at most 96 KiB; a shape that needed
+ * more would be rejected with IABN_ERR_WORKSPACE).  It allocates and frees
+ * nothing.  The scratch of the current device is used, so `stream` must
+ * belong to the current device.  All calls on one device share that
+ * scratch: calls that may overlap in time on one device (different streams,
+ * or host threads) race and must be ordered by the caller.
+ */
+int iabn_forward_train_noalloc(void *x_z, int dtype, const float *gamma, const float *beta,
+                               float *running_mean, float *running_var, float *save_mean,
+                               float *save_var, float eps, float momentum, float slope,
+                               int64_t N, int64_t C, int64_t HW, void *stream);
 
 /*
  * Inference-mode forward (Sec. 3.1, statistics fixed to the running

@@ -29,7 +29,8 @@ __all__ = [
     "iabn_workspace_size", "iabn_forward_train", "iabn_forward_eval", "iabn_backward",
     "iabn_forward_stats", "iabn_forward_apply", "iabn_backward_reduce", "iabn_backward_apply",
     "iabn_backward_ii", "iabn_std_forward_train", "iabn_std_backward", "iabn_ckpt_forward_train",
-    "iabn_ckpt_recompute", "iabn_ckpt_backward", "iabn_plan", "DTYPE_CODES", "OPS",
+    "iabn_ckpt_recompute", "iabn_ckpt_backward", "iabn_plan", "iabn_forward_train_noalloc",
+    "DTYPE_CODES", "OPS",
 ]
 
 DTYPE_CODES = {torch.float32: 0, torch.float16: 1, torch.bfloat16: 2}
@@ -84,6 +85,7 @@ def declare(lib):
         "iabn_last_error": ([], ctypes.c_char_p),
         "iabn_workspace_size": ([i64, i64, i64, i32], sz),
         "iabn_forward_train": ([vp, i32, vp, vp, vp, vp, vp, vp, f32, f32, f32, i64, i64, i64, vp, sz, vp], i32),
+        "iabn_forward_train_noalloc": ([vp, i32, vp, vp, vp, vp, vp, vp, f32, f32, f32, i64, i64, i64, vp], i32),
         "iabn_forward_eval": ([vp, i32, vp, vp, vp, vp, f32, f32, i64, i64, i64, vp], i32),
         "iabn_backward": ([vp, vp, i32, vp, vp, vp, vp, vp, f32, f32, i64, i64, i64, vp, sz, vp], i32),
         "iabn_forward_stats": ([vp, i32, i64, i64, i64, vp, sz, vp], i32),
@@ -204,6 +206,22 @@ def iabn_forward_train(x_z, gamma, beta, running_mean, running_var, save_mean, s
     rc = load().iabn_forward_train(_ptr(x_z), code, *args, float(eps), float(momentum),
                                    float(slope), N, C, HW, wp, wb, _stream(dev, stream))
     _check("iabn_forward_train", rc)
+    return x_z
+
+
+def iabn_forward_train_noalloc(x_z, gamma, beta, running_mean, running_var, save_mean, save_var,
+                               eps=1e-5, momentum=0.1, slope=0.01, stream=None):
+    """iabn_forward_train with the library's static scratch in place of a
+    workspace (no allocation, here or in the library); returns ``x_z``."""
+    N, C, HW = _nchw(x_z, "x_z")
+    code = DTYPE_CODES[x_z.dtype]
+    dev = x_z.device
+    args = [_chan(t, C, dev, n) for t, n in ((gamma, "gamma"), (beta, "beta"),
+            (running_mean, "running_mean"), (running_var, "running_var"),
+            (save_mean, "save_mean"), (save_var, "save_var"))]
+    rc = load().iabn_forward_train_noalloc(_ptr(x_z), code, *args, float(eps), float(momentum),
+                                           float(slope), N, C, HW, _stream(dev, stream))
+    _check("iabn_forward_train_noalloc", rc)
     return x_z
 
 

@@ -7,6 +7,7 @@
 #include <string.h>
 
 #include <cmath>
+#include <mutex>
 
 #include "launch.h"
 
@@ -162,11 +163,14 @@ const char* fwd_name(int fm) {
 // x is the input (kFwdInPlace: z on return; kFwdCkpt: xhat on return); out
 // receives z for kFwdOut and kFwdCkpt.  Everything is validated before the
 // first launch, so an error changes nothing.
+// ws_if_streaming: the workspace is checked only where the streaming
+// kernels run (the channel-resident ones use none); otherwise it must hold
+// iabn_workspace_size bytes whichever kernels run.
 int forward_train_impl(int fm, void* x, void* out, int dtype, const float* gamma,
                        const float* beta, float* running_mean, float* running_var,
                        float* save_mean, float* save_var, float eps, float momentum, float slope,
                        int64_t N, int64_t C, int64_t HW, void* workspace, size_t workspace_bytes,
-                       void* stream) {
+                       void* stream, bool ws_if_streaming = false) {
     int rc = validate_common(dtype, N, C, HW, true);
     if (rc) return rc;
     if (empty(N, C, HW)) return ok();
@@ -176,14 +180,17 @@ int forward_train_impl(int fm, void* x, void* out, int dtype, const float* gamma
     if ((rc = check_params(eps, slope))) return rc;
     if (!(momentum >= 0.f && momentum <= 1.f))
         return fail(IABN_ERR_PARAM, "momentum must lie in [0, 1]");
-    if ((rc = check_workspace(N, C, HW, workspace, workspace_bytes))) return rc;
     const int vec = access_vec(HW, dtype, x, fm == kFwdInPlace ? nullptr : out, nullptr);
     const Geom g = make_geom(N, C, HW, dtype, vec);
     const FwdParams prm = {gamma,    beta, running_mean, running_var, save_mean, save_var,
                            fm == kFwdInPlace ? nullptr : out, eps, momentum, slope};
     const hipStream_t st = static_cast<hipStream_t>(stream);
     FusedPlan fp;
-    if (plan_fused(C, g, elem_bytes(dtype), false, fm == kFwdInPlace, &fp)) {
+    const bool fused = plan_fused(C, g, elem_bytes(dtype), false, fm == kFwdInPlace, &fp);
+    if ((!fused || !ws_if_streaming) &&
+        (rc = check_workspace(N, C, HW, workspace, workspace_bytes)))
+        return rc;
+    if (fused) {
         if (!launch_fwd_fused(dtype, fm, x, g, fp, prm, st))
             return fail(IABN_ERR_HIP, "no %s kernel built for T=%d R=%d", fwd_name(fm), fp.T, fp.R);
         return launched(fwd_name(fm));
@@ -232,6 +239,44 @@ int backward_impl(int bm, bool ii, const void* u, const void* zs, void* dz_dx, i
     if ((rc = launched("bwd_reduce"))) return rc;
     launch_bwd_apply(dtype, vec, u, zs, dz_dx, g, static_cast<const Partial*>(part), prm, bm, st);
     return launched(bwd_name(bm, ii));
+}
+
+// ---------------------------------------------------------------- static scratch
+
+// The scratch of iabn_forward_train_noalloc: the streaming kernels' partial
+// results, in a file-scope device array instead of a caller's workspace.
+// Each device holds its own copy (zero-initialised when the library's code
+// object is loaded on it) until the process ends.  Its size bounds the
+// partials of one call: C * P slices * 4 waves * 32 bytes, at most 765
+// slices (C = 255, P = 3) where the forward takes the streaming kernels,
+// about 96 KiB.  Nothing in it needs to start at zero: every partial a call
+// reads was written by the same call.
+constexpr size_t kScratchBytes = size_t(128) << 10;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+// The device address of `scratch` on each device (null until first use),
+// taken with that device current; host code uses these, never `scratch`.
+constexpr int kMaxDevices = 64;
+void* g_scratch_addr[kMaxDevices];
+std::mutex g_scratch_mutex;
+
+int scratch_address(void** out) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return fail(IABN_ERR_HIP, "hipGetDevice: %s", hipGetErrorString(e));
+    if (dev < 0 || dev >= kMaxDevices)
+        return fail(IABN_ERR_HIP, "device %d: the scratch table holds %d devices", dev, kMaxDevices);
+    std::lock_guard<std::mutex> lock(g_scratch_mutex);
+    if (g_scratch_addr[dev] == nullptr) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || p == nullptr)
+            return fail(IABN_ERR_HIP, "hipGetSymbolAddress(scratch) on device %d: %s", dev,
+                        hipGetErrorString(e));
+        g_scratch_addr[dev] = p;
+    }
+    *out = g_scratch_addr[dev];
+    return IABN_OK;
 }
 
 }  // namespace
@@ -347,6 +392,30 @@ int iabn_forward_train(void* x_z, int dtype, const float* gamma, const float* be
     return forward_train_impl(kFwdInPlace, x_z, nullptr, dtype, gamma, beta, running_mean,
                               running_var, save_mean, save_var, eps, momentum, slope, N, C, HW,
                               workspace, workspace_bytes, stream);
+}
+
+int iabn_forward_train_noalloc(void* x_z, int dtype, const float* gamma, const float* beta,
+                               float* running_mean, float* running_var, float* save_mean,
+                               float* save_var, float eps, float momentum, float slope, int64_t N,
+                               int64_t C, int64_t HW, void* stream) {
+    int rc = validate_common(dtype, N, C, HW, true);
+    if (rc) return rc;
+    if (empty(N, C, HW)) return ok();
+    const size_t need = workspace_bytes_for(N, C, HW);
+    const int vec = access_vec(HW, dtype, x_z, nullptr, nullptr);
+    FusedPlan fp;
+    const bool fused =
+        plan_fused(C, make_geom(N, C, HW, dtype, vec), elem_bytes(dtype), false, true, &fp);
+    if (!fused && need > kScratchBytes)
+        return fail(IABN_ERR_WORKSPACE,
+                    "this shape needs %zu bytes of scratch, more than the %zu the library "
+                    "holds per device",
+                    need, kScratchBytes);
+    void* ws = nullptr;
+    if ((rc = scratch_address(&ws))) return rc;
+    return forward_train_impl(kFwdInPlace, x_z, nullptr, dtype, gamma, beta, running_mean,
+                              running_var, save_mean, save_var, eps, momentum, slope, N, C, HW, ws,
+                              kScratchBytes, stream, true);
 }
 
 int iabn_forward_eval(void* x_z, int dtype, const float* gamma, const float* beta,

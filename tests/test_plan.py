@@ -130,3 +130,21 @@ def test_empty_and_invalid():
     assert e.value.status == 4
     lib = iabn.load()
     assert lib.iabn_plan(0, 1, 2, 4, 4, None) == 1
+
+
+def test_forward_streaming_partials_fit_the_static_scratch():
+    """The training forward takes the streaming kernels (the only ones with a
+    scratch buffer) only below 256 channels, where a call's partials never
+    exceed 96 KiB: iabn_forward_train_noalloc's 128 KiB scratch holds every
+    shape."""
+    for C in (256, 300, 1024, 8192, 1 << 20):
+        for N, HW in ((1, 2), (8, 4096), (2, 1 << 20)):
+            if C * N * HW <= 1 << 46:
+                p = iabn.iabn_plan("forward_train", torch.float16, N, C, HW)
+                assert p["channel_resident"] == 1, (N, C, HW)
+    worst = 0
+    for C in range(1, 256):
+        for N, HW in ((1, 2), (2, 4096), (8, 65536), (64, 1 << 20)):
+            worst = max(worst, iabn.iabn_workspace_size(N, C, HW, torch.float16))
+    assert worst <= 96 * 1024, worst
+    assert worst == 765 * 4 * 32  # C = 255: 3 slices per channel, 4 partials of 32 bytes each
