@@ -122,9 +122,11 @@ typedef struct {
 } iabn_plan_t;
 
 /* The kernels entry point `op` (an iabn_op_t) runs for this shape and
- * storage type, with every tensor 16-byte aligned (a tensor that is not can
- * only make the accesses narrower).  Host only: needs no GPU, launches
- * nothing.  For callers that schedule around the library, and for tests of
+ * storage type when every tensor is 16-byte aligned.  The plan holds only
+ * for such tensors: a tensor that is not takes narrower accesses, which can
+ * change every field (the comparison blocks then take the streaming kernels,
+ * InPlace-ABN's own entry points other rungs and block sizes).  Host only:
+ * needs no GPU, launches nothing.  For callers that schedule around the library, and for tests of
  * the library's choices.  Validates like the entry point (shape, dtype; a
  * NULL plan is IABN_ERR_NULL, an unknown op IABN_ERR_PARAM); an empty shape
  * gives an all-zero plan. */

@@ -42,8 +42,13 @@ def _load():
     global _lib
     if _lib is not None:
         return _lib
-    build(force=False)
-    lib = ctypes.CDLL(_LIB)
+    # Another build of the same source (the sanitizer build of the tests),
+    # loaded instead of the default library when named.
+    path = os.environ.get("IABN_ORACLE_LIB")
+    if not path:
+        build(force=False)
+        path = _LIB
+    lib = ctypes.CDLL(path)
     P = ctypes.POINTER(ctypes.c_double)
     I = ctypes.c_int64
     D = ctypes.c_double

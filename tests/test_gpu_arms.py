@@ -21,6 +21,7 @@ import oracle
 import paper_1712_02616_amd as iabn
 import workloads
 from gpu_helpers import TORCH_DTYPES, TOL, assert_close, max_rel, say, to_device, to_f64
+from chain_allowance import check_same_inputs
 from test_gpu_parity import (ALL_CASES, CONFIG_CASES, EDGE_CASES, F32, STORE_U, Case,
                              chain_allowances, check_chain, make_inputs, oracle_forward)
 
@@ -285,6 +286,10 @@ def test_std_chain_parity(case):
     allow = chain_allowances(fw["z"], dz, bw, fw["var"], inp.gamma, inp.beta, case.eps,
                              case.slope, case.dtype, flip)
     check_chain(to_f64(g), to_f64(D.dgamma), to_f64(D.dbeta), bw, allow, flip, case.dtype)
+    # The backward against the oracle's on the forward's own x, z and statistics.
+    same = oracle.backward_standard(f64(inp.x, case.dtype), dz, inp.gamma, inp.beta, to_f64(D.mean),
+                                    to_f64(D.var), F32(case.eps), F32(case.slope), z=to_f64(z))
+    check_same_inputs(to_f64(g), to_f64(D.dgamma), to_f64(D.dbeta), same, case.dtype)
 
 
 @pytest.mark.parametrize("case", CHAIN_CASES, ids=lambda c: c.id)
@@ -322,6 +327,10 @@ def test_ckpt_chain_parity(case):
     allow = chain_allowances(z_equiv, dz, bw, fw["var"], inp.gamma, np.zeros_like(inp.beta),
                              case.eps, case.slope, case.dtype, flip)
     check_chain(to_f64(g), to_f64(D.dgamma), to_f64(D.dbeta), bw, allow, flip, case.dtype)
+    # The backward against the oracle's on the forward's own stored xhat and sigma^2.
+    same = oracle.backward_from_xhat(to_f64(xh), dz, inp.gamma, inp.beta, to_f64(D.var),
+                                     F32(case.eps), F32(case.slope))
+    check_same_inputs(to_f64(g), to_f64(D.dgamma), to_f64(D.dbeta), same, case.dtype)
 
 
 # ---------------------------------------------------------------- full size, sampled
@@ -361,6 +370,10 @@ def test_backbone_layer_arms_sampled(layer):
     allow = chain_allowances(fw["z"], dz64, bw, fw["var"], gc, bc, w.eps, w.slope, w.dtype, flip)
     check_chain(to_f64(g[:, chans]), to_f64(D.dgamma)[chans], to_f64(D.dbeta)[chans], bw, allow,
                 flip, w.dtype)
+    same = oracle.backward_standard(x64, dz64, gc, bc, to_f64(D.mean)[chans], to_f64(D.var)[chans],
+                                    F32(w.eps), F32(w.slope), z=zc)
+    check_same_inputs(to_f64(g[:, chans]), to_f64(D.dgamma)[chans], to_f64(D.dbeta)[chans], same,
+                      w.dtype)
     # checkpointing
     D = Dev(inp)
     xh = to_device(inp.x, w.dtype)
@@ -388,6 +401,10 @@ def test_backbone_layer_arms_sampled(layer):
                              w.dtype, flip)
     check_chain(to_f64(g[:, chans]), to_f64(D.dgamma)[chans], to_f64(D.dbeta)[chans], bw, allow,
                 flip, w.dtype)
+    same = oracle.backward_from_xhat(to_f64(xh[:, chans]), dz64, gc, bc, to_f64(D.var)[chans],
+                                     F32(w.eps), F32(w.slope))
+    check_same_inputs(to_f64(g[:, chans]), to_f64(D.dgamma)[chans], to_f64(D.dbeta)[chans], same,
+                      w.dtype)
     # InPlace-ABN II, from the InPlace-ABN forward's z
     D = Dev(inp)
     xz = to_device(inp.x, w.dtype)
@@ -403,6 +420,9 @@ def test_backbone_layer_arms_sampled(layer):
     allow = chain_allowances(fw["z"], dz64, bw, fw["var"], gc, bc, w.eps, w.slope, w.dtype, flip)
     check_chain(to_f64(g[:, chans]), to_f64(D.dgamma)[chans], to_f64(D.dbeta)[chans], bw, allow,
                 flip, w.dtype)
+    same = oracle.backward_ii(zc, dz64, gc, bc, to_f64(D.var)[chans], F32(w.eps), F32(w.slope))
+    check_same_inputs(to_f64(g[:, chans]), to_f64(D.dgamma)[chans], to_f64(D.dbeta)[chans], same,
+                      w.dtype)
 
 
 # ---------------------------------------------------------------- determinism and errors

@@ -13,9 +13,10 @@ Per layer and path:
             to fp16) and the same sigma^2; dx element by element, dgamma and
             dbeta per channel, at the fp16 gate and with no allowance; z is
             read-only.
-  chain     GPU forward then GPU backward in place against the oracle's
-            exact chain, with the kink and storage-rounding allowances of
-            ``chain_allowances``.
+  chain     GPU forward then GPU backward in place: against the oracle's
+            backward on the GPU forward's own stored z and sigma^2 at the
+            gate, and against the oracle's exact chain with the kink and
+            storage-rounding allowances of ``chain_allowances``.
 
 Channels are independent, so the oracle runs over chunks of channels (host
 memory stays bounded); relative errors are floored at 1e-3 of the maximum
@@ -31,6 +32,7 @@ import torch
 import oracle
 import workloads
 from gpu_helpers import TOL, GpuLayer, say, to_device, to_f64
+from chain_allowance import check_same_inputs
 from test_gpu_parity import F32, PATHS, chain_allowances, check_chain
 
 pytestmark = [pytest.mark.gpu,
@@ -174,3 +176,14 @@ def test_backbone_layer_whole(layer, path):
                     allow, flip, W5.dtype, scales=scales)
     say("  chain: %d kink flips of %d elements" % (nflip, N * C * HW))
     assert nflip <= max(8, 1e-5 * N * C * HW)
+    del ref
+
+    # The chain's backward against the oracle's on the GPU forward's own z and sigma^2.
+    say("backbone whole layer %d %s: oracle backward (the GPU's stored z)" % (layer, path))
+    same = oracle_backward_chunked(z_gpu.astype(np.float64), inp.dz, inp.gamma, inp.beta,
+                                   stats["var"], eps, slope)
+    scales = {k: np.abs(same[k]).max() for k in ("dx", "dgamma", "dbeta")}
+    for c0, c1 in chunks(N, C, HW):
+        sub = {k: same[k][c0:c1] if k != "dx" else same["dx"][:, c0:c1] for k in same}
+        check_same_inputs(dx_chain[:, c0:c1].astype(np.float64), dg_chain[c0:c1], db_chain[c0:c1],
+                          sub, W5.dtype, scales=scales)

@@ -34,6 +34,8 @@ import torch
 import oracle
 import paper_1712_02616_amd as iabn
 import workloads
+from chain_allowance import (STORE_ABS, STORE_U, chain_allowances, check_chain,  # noqa: F401
+                             check_same_inputs)
 from gpu_helpers import GpuLayer, TORCH_DTYPES, TOL, assert_close, max_rel, say, to_device, to_f64
 
 pytestmark = [pytest.mark.gpu,
@@ -206,67 +208,11 @@ def test_chain_parity(case, path):
                              case.slope, case.dtype, flip)
     check_chain(to_f64(L.dz).reshape(bw["dx"].shape), to_f64(L.dgamma), to_f64(L.dbeta), bw, allow,
                 flip, case.dtype)
-
-
-# Unit roundoff of the stored z, plus a few fp32 roundings of the kernel's y
-# before the store; and the absolute half-ulp below which a*y flushes into
-# fp16 subnormals / zero.
-STORE_U = {"f32": 4 * 2.0 ** -24, "f16": 2.0 ** -11 + 4 * 2.0 ** -24,
-           "bf16": 2.0 ** -8 + 4 * 2.0 ** -24}
-STORE_ABS = {"f32": 2.0 ** -150, "f16": 2.0 ** -25, "bf16": 2.0 ** -134}
-
-
-def chain_allowances(z_ref, dz, ref, var, gamma, beta, eps, slope, dtype, flip):
-    """What a forward + backward chain with z kept in the storage type may
-    differ from the exact-arithmetic chain by, beyond the tolerance.
-
-    - Elements that took the other branch at the kink (``flip``) change dbeta
-      by (1 - a) dz_i and dgamma by (1 - a) dz_i xhat_i, with |y_i| <= 1 there.
-    - The backward recovers xhat from the stored z.  With unit roundoff u of
-      the storage type, |y_stored - y| <= u |y| + h/a (h: half the smallest
-      subnormal step), so delta_i = |xhat_stored_i - xhat_i| <= (u |y_i| + h/a)/|gamma|,
-      dgamma = sum dy xhat moves by at most D = sum |dy_i| delta_i, and
-      dx_i = A (dy_i - dgamma xhat_i/m - dbeta/m) by at most
-      |A|/m (|dgamma| delta_i + D (|xhat_i| + delta_i)) (first order).
-    Returns (dx, dgamma, dbeta) allowances.
-    """
-    g = np.asarray(gamma, np.float64)[None, :, None]
-    b = np.asarray(beta, np.float64)[None, :, None]
-    a = F32(slope)
-    m = z_ref.shape[0] * z_ref.shape[2]
-    y = np.where(z_ref >= 0, z_ref, z_ref / a)
-    dy = np.where(z_ref >= 0, dz, a * dz)
-    xhat = (y - b) / g
-    delta = (STORE_U[dtype] * np.abs(y) + STORE_ABS[dtype] / a) / np.abs(g)
-    flipped = np.abs(np.where(flip, dz, 0.0))
-    slack_b = flipped.sum(axis=(0, 2))
-    slack_g = (flipped * (np.abs(b) + 1.0) / np.abs(g)).sum(axis=(0, 2))
-    D = (np.abs(dy) * delta).sum(axis=(0, 2))
-    slack_g = slack_g + D
-    A = np.abs(g) / np.sqrt(np.asarray(var, np.float64)[None, :, None] + F32(eps))
-    dg = np.abs(ref["dgamma"])[None, :, None]
-    slack_dx = A / m * (dg * delta + (D + slack_b)[None, :, None] * (np.abs(xhat) + delta + 1.0))
-    return slack_dx, slack_g, slack_b
-
-
-def check_chain(dx, dgamma, dbeta, ref, allow, flip, dtype, scales=None):
-    """``scales``: the max |ref| of dx, dgamma and dbeta over the whole tensor
-    when ``ref`` covers only some of its channels (the relative error's floor
-    is 1e-3 of that); by default the maxima over ``ref`` itself."""
-    slack_dx, slack_g, slack_b = allow
-    keep = ~flip
-    sc = scales or {k: np.abs(ref[k]).max() for k in ("dx", "dgamma", "dbeta")}
-    floor = np.maximum(np.abs(ref["dx"]), 1e-3 * sc["dx"])
-    err = np.abs(dx - ref["dx"]) - slack_dx
-    assert np.all(np.isfinite(dx)), "dx has non-finite values"
-    worst = float(np.max((err / floor)[keep])) if keep.any() else 0.0
-    assert worst <= TOL[dtype], "dx: max rel err beyond allowance %.3e > %.1e" % (worst, TOL[dtype])
-    for name, got, r, slack in (("dbeta", dbeta, ref["dbeta"], slack_b),
-                                ("dgamma", dgamma, ref["dgamma"], slack_g)):
-        fl = np.maximum(np.abs(r), 1e-3 * sc[name])
-        bad = np.abs(got - r) > TOL[dtype] * fl + slack
-        assert not bad.any(), "%s: channels %s got %s ref %s slack %s" % (
-            name, np.nonzero(bad)[0][:5], got[bad][:5], r[bad][:5], slack[bad][:5])
+    # The backward against the oracle's on the GPU forward's own z and sigma^2.
+    same = oracle.backward_i(zg, dz, inp.gamma, inp.beta, to_f64(L.save_var), F32(case.eps),
+                             F32(case.slope))
+    check_same_inputs(to_f64(L.dz).reshape(bw["dx"].shape), to_f64(L.dgamma), to_f64(L.dbeta), same,
+                      case.dtype)
 
 
 @pytest.mark.parametrize("case", [CONFIG_CASES[0], EDGE_CASES[0], EDGE_CASES[6], CONFIG_CASES[3]] +
@@ -363,6 +309,9 @@ def test_guard_band_and_alignment(dtype, offset, C):
     allow = chain_allowances(fw["z"], dzf, bw, fw["var"], inp.gamma, inp.beta, case.eps, case.slope,
                              dtype, flip)
     check_chain(to_f64(dz), to_f64(L.dgamma), to_f64(L.dbeta), bw, allow, flip, dtype)
+    same = oracle.backward_i(zg, dzf, inp.gamma, inp.beta, to_f64(L.save_var), F32(case.eps),
+                             F32(case.slope))
+    check_same_inputs(to_f64(dz), to_f64(L.dgamma), to_f64(L.dbeta), same, dtype)
 
 
 def test_errors_leave_outputs_untouched():
@@ -426,3 +375,6 @@ def test_backbone_layer_sampled(layer, path):
     allow = chain_allowances(fw["z"], dz, bw, fw["var"], inp.gamma[chans], inp.beta[chans], w.eps,
                              w.slope, w.dtype, flip)
     check_chain(dxc, to_f64(L.dgamma)[chans], to_f64(L.dbeta)[chans], bw, allow, flip, w.dtype)
+    same = oracle.backward_i(zc, dz, inp.gamma[chans], inp.beta[chans], to_f64(L.save_var)[chans],
+                             F32(w.eps), F32(w.slope))
+    check_same_inputs(dxc, to_f64(L.dgamma)[chans], to_f64(L.dbeta)[chans], same, w.dtype)

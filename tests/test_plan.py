@@ -148,3 +148,17 @@ def test_forward_streaming_partials_fit_the_static_scratch():
             worst = max(worst, iabn.iabn_workspace_size(N, C, HW, torch.float16))
     assert worst <= 96 * 1024, worst
     assert worst == 765 * 4 * 32  # C = 255: 3 slices per channel, 4 partials of 32 bytes each
+
+
+def test_narrower_accesses_change_the_plan():
+    """iabn_plan describes 16-byte-aligned tensors.  A tensor that is not
+    (say 8 bytes off) takes the accesses a row that only 8-byte accesses
+    divide takes, and that changes the plan, not only its access width: the
+    standard block leaves the channel-resident kernels, InPlace-ABN's forward
+    takes another rung.  (8, 1024, 4100) fp16 has such rows; the aligned
+    neighbour (8, 1024, 4096) does not."""
+    fused(plan("std_forward", F16, 8, 1024, 4096), 256, 16, strips=1)
+    streaming(plan("std_forward", F16, 8, 1024, 4100), access=8, xcd=1)
+    streaming(plan("std_backward", F16, 8, 1024, 4100), access=8, xcd=1)
+    fused(plan("forward_train", F16, 8, 1024, 4096), 256, 16, strips=1)
+    fused(plan("forward_train", F16, 8, 1024, 4100), 1024, 16, lds=0, access=8, xcd=1)
