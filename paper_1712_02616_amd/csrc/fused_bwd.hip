@@ -26,16 +26,6 @@ __device__ __forceinline__ void bwd_fused_channel(const void* __restrict__ u,
     const uint64_t cbase = static_cast<uint64_t>(c) * g.vrow;
     const uint32_t tid = threadIdx.x;
     const uint32_t nstrips = STRIP ? g.vchan / T : 0;
-    // All per-channel inputs first: a load issued after the data loads would
-    // put another memory round trip after the reduction barrier.
-    const float gamma_c = prm.gamma[c], beta_c = prm.beta[c], var_c = prm.save_var[c];
-    const float mean_c = XZ ? prm.save_mean[c] : 0.f;
-    const double invstd =
-        1.0 / sqrt(static_cast<double>(var_c) + static_cast<double>(prm.eps));
-    const BwdReduceElem<BM> el =
-        make_reduce_elem<BM>(prm.slope, gamma_c, beta_c, mean_c, invstd, prm.ii != 0);
-    const BwdRecip rc = make_recip(gamma_c, prm.slope, g.inv_m);
-
     // Register-resident accesses non-temporal, the rest cached (see
     // fwd_fused_channel).  kBwdFromXZ first loads z (into the registers x
     // will use) and dz, turns z into sign bits, and only then loads x, so
@@ -51,6 +41,21 @@ __device__ __forceinline__ void bwd_fused_channel(const void* __restrict__ u,
     uint32_t negm[NW];
 #pragma unroll
     for (int q = 0; q < NW; ++q) negm[q] = 0u;
+    float gamma_c, beta_c, mean_c;
+    double invstd;
+    BwdReduceElem<BM> el;
+    BwdRecip rc;
+    auto channel_inputs = [&]() {
+        gamma_c = prm.gamma[c];
+        beta_c = prm.beta[c];
+        const float var_c = prm.save_var[c];
+        mean_c = XZ ? prm.save_mean[c] : 0.f;
+        invstd = 1.0 / sqrt(static_cast<double>(var_c) + static_cast<double>(prm.eps));
+        el = make_reduce_elem<BM>(prm.slope, gamma_c, beta_c, mean_c, invstd, prm.ii != 0);
+        rc = make_recip(gamma_c, prm.slope, g.inv_m);
+    };
+    if constexpr (XZ) channel_inputs();
+    // Index of the thread's k-th resident access (live: within the channel).
     auto resident_index = [&](int k, StripPos& p, bool& live) -> uint64_t {
         if constexpr (STRIP) {
             const uint64_t i = p.off + tid;
@@ -97,16 +102,31 @@ __device__ __forceinline__ void bwd_fused_channel(const void* __restrict__ u,
             if (live) ku[k] = load_raw<DT, VEC, kStream>(u, i1);
         }
     } else {
+        // Slots past the channel (general mapping) read the channel's first
+        // access instead, a line the block reads anyway, and are never used:
+        // loads under a condition can make the compiler carry the whole
+        // register buffer through every join, copying it after each load and
+        // so waiting for each load in turn.  (The standard block's mode above
+        // keeps its conditional loads, which need fewer registers there.)
 #pragma unroll
         for (int k = 0; k < R; ++k) {
             bool live;
-            const uint64_t i1 = resident_index(k, sp, live);
-            if (live) {
-                ku[k] = load_raw<DT, VEC, kStream>(u, i1);
-                kg[k] = load_raw<DT, VEC, kStream>(dzdx, i1);
-            }
+            const uint64_t i1 = STRIP ? resident_index(k, sp, live)
+                                      : access_index(g, cbase, tid + k * T < g.vchan ? tid + k * T : 0);
+            ku[k] = load_raw<DT, VEC, kStream>(u, i1);
+            kg[k] = load_raw<DT, VEC, kStream>(dzdx, i1);
         }
     }
+    // The per-channel inputs, read once the data loads are out: their round
+    // trip then overlaps the data's (read before the data loads, every wave
+    // waited for them before issuing its own), and they have arrived before
+    // the first data does.  (The standard block's backward reads them first:
+    // it holds three tensors, and reading them later costs it registers.)
+    if constexpr (!XZ) {
+        sched_fence();
+        channel_inputs();
+    }
+
     // fp32 within one access, fp64 across accesses (as the streaming reduce
     // does per unrolled step): a channel's sums of dy cancel to near zero and
     // an fp32 running sum over the whole register-resident part loses that.

@@ -98,14 +98,6 @@ __device__ __forceinline__ void fwd_fused_channel(void* __restrict__ xz, const G
     const uint64_t cbase = static_cast<uint64_t>(c) * g.vrow;
     const uint32_t tid = threadIdx.x;
     const uint32_t nstrips = STRIP ? g.vchan / T : 0;
-    // Per-channel inputs before the data loads (see bwd_fused_channel).
-    const float gamma_c = prm.gamma[c], beta_c = prm.beta[c];
-    float rm_c = 0.f, rv_c = 0.f;
-    if (tid == 0) {
-        rm_c = prm.running_mean[c];
-        rv_c = prm.running_var[c];
-    }
-
     // The first R accesses per thread stay in registers until the apply, so
     // this is their only read: non-temporal.  Accesses past those are read
     // again by the apply and go through the caches.  (Measured: non-temporal
@@ -124,10 +116,23 @@ __device__ __forceinline__ void fwd_fused_channel(void* __restrict__ xz, const G
             keep[k] = load_raw<DT, VEC, kStream>(xz, sp.off + tid);
             strip_next<T>(g, sp);
         } else {
+            // Slots past the channel read its first access instead (a line
+            // the block reads anyway) and are not used: loads under a
+            // condition make the compiler carry the whole buffer through
+            // every join, copying it after each load.
             const uint32_t v = tid + k * T;
-            if (v < g.vchan) keep[k] = load_raw<DT, VEC, kStream>(xz, access_index(g, cbase, v));
+            keep[k] = load_raw<DT, VEC, kStream>(xz, access_index(g, cbase, v < g.vchan ? v : 0));
         }
     }
+    // The per-channel inputs are read once the data loads are out (see
+    // bwd_fused_channel), and waited for here, while the data is still on
+    // its way (left to the compiler, the loads sink to their first use after
+    // the data has arrived, and their round trip is paid then).
+    sched_fence();
+    const float gamma_c = prm.gamma[c], beta_c = prm.beta[c];
+    const float rm_c = prm.running_mean[c], rv_c = prm.running_var[c];
+    asm volatile("" ::"s"(gamma_c), "s"(beta_c), "s"(rm_c), "s"(rv_c));
+    sched_fence();
     float shift = 0.f, s1 = 0.f, s2 = 0.f;
     uint32_t nacc = 0;
     if (tid < g.vchan) {
@@ -259,12 +264,14 @@ bool launch_v(void* xz, const Geom& g, const FusedPlan& fp, const FwdParams& prm
     if constexpr (V * sizeof(typename Elem<DT>::T) == 16) {
         IABN_FUSED_CASE(256, 4)
         IABN_FUSED_CASE(256, 8)
+        IABN_FUSED_CASE(64, 32)
         IABN_FUSED_CASE(256, 16)
         IABN_FUSED_CASE(512, 16)
         IABN_FUSED_CASE(1024, 16)
     } else if constexpr (FM == kFwdInPlace) {
         IABN_FUSED_CASE_GENERAL(256, 4)
         IABN_FUSED_CASE_GENERAL(256, 8)
+        IABN_FUSED_CASE_GENERAL(64, 32)
         IABN_FUSED_CASE_GENERAL(512, 4)
         IABN_FUSED_CASE_GENERAL(256, 16)
         IABN_FUSED_CASE_GENERAL(512, 16)

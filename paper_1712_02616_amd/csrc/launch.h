@@ -117,6 +117,18 @@ constexpr FusedPlan kNarrowLadder[] = {{256, 4}, {256, 8}, {256, 16}, {512, 16},
 constexpr FusedPlan kNarrowLadderFew[] = {{256, 4}, {512, 4}, {256, 16}, {512, 16}, {1024, 16}};
 static_assert(sizeof kNarrowLadderFew == sizeof kNarrowLadder, "the narrow ladders have one length");
 
+// With at least two channels per SIMD (2048 on 1024 SIMDs), the forward's
+// channels of 1025-2048 accesses take one wave each instead of (256, 8):
+// each wave then reduces and writes its channel without waiting for other
+// waves at a block barrier.  Measured: (16, 2048, 28x28) bf16 forward 19.7 us
+// against 22.2, (8, 2048, 28x28) fp32 18.1 against 21.1, (32, 2048, 14x14)
+// fp16 (8-byte accesses) 13.3 against 14.0; with fewer channels it is
+// slower ((16, 1024, 28x28) fp16 12.6 against 11.0, (8, 300, 32x64) fp16
+// 9.8 against 6.8).  The backward's two tensors do not fit one wave's
+// registers ((128, 16) measured slower than (256, 8) there).
+constexpr int64_t kOneWaveMinChannels = 2048;
+constexpr FusedPlan kOneWaveRung = {64, 32};
+
 // elem_bytes: storage size; narrow_ok: whether this entry point has narrow
 // channel-resident kernels.
 inline bool plan_fused(int64_t C, const Geom& g, int elem_bytes, bool backward, bool narrow_ok,
@@ -134,6 +146,8 @@ inline bool plan_fused(int64_t C, const Geom& g, int elem_bytes, bool backward, 
     for (int i = 0; i < n; ++i) {
         if (A <= static_cast<int64_t>(ladder[i].T) * ladder[i].R || i == n - 1) {
             *out = ladder[i];
+            if (!backward && C >= kOneWaveMinChannels && out->T == 256 && out->R == 8)
+                *out = kOneWaveRung;
             return true;
         }
     }

@@ -117,6 +117,11 @@ EDGE_CASES = [
     Case("narrow4_rung512_f16", 128, 256, 98, "f16", 39, dz_std=0.1),
     Case("narrow8_few_c200_f16", 32, 200, 196, "f16", 47, dz_std=0.1, gamma_sign=True),
     Case("narrow2_few_c256_bf16", 32, 256, 49, "bf16", 48, dz_std=0.1),
+    # One wave per channel in the forward (2048+ channels of 1025-2048
+    # accesses): general mapping fp32, strips fp16, 8-byte accesses.
+    Case("onewave_c2048_f32", 8, 2048, 784, "f32", 49, gamma_sign=True),
+    Case("onewave_strip_c2048_f16", 2, 2048, 8192, "f16", 50, dz_std=0.1),
+    Case("onewave_narrow8_c2048_f16", 32, 2048, 196, "f16", 51, dz_std=0.1, gamma_sign=True),
 ]
 ALL_CASES = CONFIG_CASES + EDGE_CASES
 

@@ -53,8 +53,10 @@ def test_parity_workloads():
     fused(plan("backward", F32, 32, 256, 56 * 56), 1024, 11, lds=4, strips=0)
     # Segmentation crop: 18432 accesses, two strips past the forward's registers.
     fused(plan("forward_train", F16, 4, 256, 192 * 192), 1024, 16, lds=2, strips=0)
-    # Wide layer: 1568 accesses per channel, rows of 1568 bytes (not whole lines).
-    fused(plan("forward_train", BF16, 16, 2048, 28 * 28), 256, 8, strips=0, xcd=1, blocks=2048)
+    # Wide layer: 1568 accesses per channel, rows of 1568 bytes (not whole
+    # lines); 2048 channels: the forward takes one wave per channel.
+    fused(plan("forward_train", BF16, 16, 2048, 28 * 28), 64, 32, strips=0, xcd=1, blocks=2048)
+    fused(plan("backward", BF16, 16, 2048, 28 * 28), 256, 8, strips=0, xcd=1, blocks=2048)
     # Tiny layer: streaming.
     streaming(plan("forward_train", F32, 2, 16, 8 * 8))
 
@@ -81,7 +83,26 @@ def test_rungs():
     # Narrow rows with at most one channel per CU: (512, 4); with more: (256, 8).
     fused(plan("backward", F16, 32, 200, 14 * 14), 512, 4, access=8, xcd=1)
     fused(plan("backward", F16, 32, 1024, 14 * 14), 256, 8, access=8, xcd=1)
-    fused(plan("forward_train", F16, 32, 2048, 7 * 7), 256, 8, access=2, xcd=1)
+    fused(plan("forward_train", F16, 32, 1024, 7 * 7), 256, 8, access=2, xcd=1)
+    fused(plan("forward_train", F16, 32, 2048, 7 * 7), 64, 32, access=2, xcd=1)
+
+
+def test_one_wave_rung():
+    """From 2048 channels (two per SIMD) the forward's 1025-2048-access
+    channels take one wave each, on every access width; the backward keeps
+    (256, 8)."""
+    fused(plan("forward_train", F16, 16, 2047, 28 * 28), 256, 8, xcd=1)
+    fused(plan("forward_train", F16, 16, 2048, 28 * 28), 64, 32, xcd=1)
+    fused(plan("forward_train", F32, 8, 2048, 28 * 28), 64, 32, xcd=1)
+    fused(plan("forward_train", F16, 2, 2048, 8192), 64, 32, strips=1)
+    fused(plan("std_forward", F16, 16, 4096, 28 * 28), 64, 32, xcd=1)
+    fused(plan("ckpt_forward", F16, 16, 4096, 28 * 28), 64, 32, xcd=1)
+    fused(plan("forward_train", F16, 32, 2048, 14 * 14), 64, 32, access=8, xcd=1)
+    fused(plan("backward", F16, 32, 2048, 14 * 14), 256, 8, access=8, xcd=1)
+    fused(plan("std_backward", F16, 16, 2048, 28 * 28), 256, 8, xcd=1)
+    # Other rungs are unchanged.
+    fused(plan("forward_train", F16, 8, 2048, 64 * 64), 256, 16, strips=1)
+    fused(plan("forward_train", F16, 8, 2048, 32 * 32), 256, 4, strips=0)
 
 
 def test_comparison_blocks():
