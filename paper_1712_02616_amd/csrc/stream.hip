@@ -36,10 +36,32 @@
 // combines run in a fixed order, so results are bit-identical from run to
 // run.
 
+#include "fused.h"
 #include "launch.h"
 
 namespace iabn_impl {
 namespace {
+
+// Index of access v of a slice's last, partial batch: accesses at or past
+// the slice's end read the slice's first access instead (a line the block
+// reads anyway) and are not used.  Loading every access of the batch
+// unconditionally keeps all of them in flight at once; one at a time, a
+// short slice of narrow accesses waited for each load in turn.
+__device__ __forceinline__ uint64_t rest_index(const Geom& g, uint64_t cbase, const Slice& s,
+                                               uint32_t v) {
+    return access_index(g, cbase, v < s.hi ? v : s.lo);
+}
+
+// The accesses of a batch are loaded raw, all of them, before any is
+// widened to fp32 (sched_fence between): left to itself the compiler
+// interleaves each conversion, and the wait it needs, with the next load,
+// which on narrow accesses (a dozen or more per batch) left one load in
+// flight at a time.
+template <int DT, int VEC, int U>
+__device__ __forceinline__ void widen(const raw_t<DT, VEC> (&r)[U], float (&t)[U][VEC]) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) unpack<DT, VEC>(r[u], t[u]);
+}
 
 // ---------------------------------------------------------------- forward
 
@@ -60,10 +82,13 @@ __global__ __launch_bounds__(kThreads) void fwd_stats_kernel(const void* __restr
     uint32_t nacc = 0;
     uint32_t v = s.lo + threadIdx.x;
     for (; v + (U - 1) * kThreads < s.hi; v += U * kThreads) {
-        float t[U][VEC];
+        raw_t<DT, VEC> r[U];
 #pragma unroll
         for (int u = 0; u < U; ++u)
-            load_vec<DT, VEC, kHintStatsLoad>(x, access_index(g, cbase, v + u * kThreads), t[u]);
+            r[u] = load_raw<DT, VEC, kHintStatsLoad>(x, access_index(g, cbase, v + u * kThreads));
+        sched_fence();
+        float t[U][VEC];
+        widen<DT, VEC, U>(r, t);
         if (first) shift = t[0][0];
         first = false;
         float a1 = 0.f, a2 = 0.f;
@@ -80,18 +105,30 @@ __global__ __launch_bounds__(kThreads) void fwd_stats_kernel(const void* __restr
         s2 += a2;
         nacc += U;
     }
-    for (; v < s.hi; v += kThreads) {
-        float t[VEC];
-        load_vec<DT, VEC, kHintStatsLoad>(x, access_index(g, cbase, v), t);
-        if (first) shift = t[0];
-        first = false;
+    // The last, partial batch: every load in flight at once (accesses past
+    // the slice read its first access instead and are not used; see
+    // rest_index).
+    if (v < s.hi) {
+        raw_t<DT, VEC> r[U];
 #pragma unroll
-        for (int k = 0; k < VEC; ++k) {
-            const float d = t[k] - shift;
-            s1 += d;
-            s2 = fmaf(d, d, s2);
+        for (int u = 0; u < U; ++u)
+            r[u] = load_raw<DT, VEC, kHintStatsLoad>(x, rest_index(g, cbase, s, v + u * kThreads));
+        sched_fence();
+        float t[U][VEC];
+        widen<DT, VEC, U>(r, t);
+        if (first) shift = t[0][0];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            if (v + u * kThreads < s.hi) {
+#pragma unroll
+                for (int k = 0; k < VEC; ++k) {
+                    const float d = t[u][k] - shift;
+                    s1 += d;
+                    s2 = fmaf(d, d, s2);
+                }
+                nacc += 1;
+            }
         }
-        nacc += 1;
     }
     // Lane 0 has the smallest index of its wave, so if it read nothing the
     // whole wave read nothing and its sums are zero.
@@ -127,14 +164,14 @@ __global__ __launch_bounds__(kThreads) void fwd_apply_kernel(void* __restrict__ 
 
     // First batch in flight before the per-channel coefficients are known.
     uint32_t v = s.lo + threadIdx.x;
-    float t[U][VEC];
+    raw_t<DT, VEC> r[U];
     uint64_t idx[U];
     bool full = v + (U - 1) * kThreads < s.hi;
     if (full) {
 #pragma unroll
         for (int q = 0; q < U; ++q) {
             idx[q] = access_index(g, cbase, v + q * kThreads);
-            load_vec<DT, VEC, kHintFwdApplyLoad>(xz, idx[q], t[q]);
+            r[q] = load_raw<DT, VEC, kHintFwdApplyLoad>(xz, idx[q]);
         }
     }
 
@@ -187,6 +224,8 @@ __global__ __launch_bounds__(kThreads) void fwd_apply_kernel(void* __restrict__ 
     };
 
     while (full) {
+        float t[U][VEC];
+        widen<DT, VEC, U>(r, t);
 #pragma unroll
         for (int q = 0; q < U; ++q) emit(t[q], idx[q]);
         v += U * kThreads;
@@ -195,15 +234,21 @@ __global__ __launch_bounds__(kThreads) void fwd_apply_kernel(void* __restrict__ 
 #pragma unroll
             for (int q = 0; q < U; ++q) {
                 idx[q] = access_index(g, cbase, v + q * kThreads);
-                load_vec<DT, VEC, kHintFwdApplyLoad>(xz, idx[q], t[q]);
+                r[q] = load_raw<DT, VEC, kHintFwdApplyLoad>(xz, idx[q]);
             }
+            sched_fence();
         }
     }
-    for (; v < s.hi; v += kThreads) {
-        float r[VEC];
-        const uint64_t i1 = access_index(g, cbase, v);
-        load_vec<DT, VEC, kHintFwdApplyLoad>(xz, i1, r);
-        emit(r, i1);
+    if (v < s.hi) {
+#pragma unroll
+        for (int q = 0; q < U; ++q)
+            r[q] = load_raw<DT, VEC, kHintFwdApplyLoad>(xz, rest_index(g, cbase, s, v + q * kThreads));
+        sched_fence();
+        float t[U][VEC];
+        widen<DT, VEC, U>(r, t);
+#pragma unroll
+        for (int q = 0; q < U; ++q)
+            if (v + q * kThreads < s.hi) emit(t[q], access_index(g, cbase, v + q * kThreads));
     }
 }
 
@@ -231,15 +276,38 @@ __global__ __launch_bounds__(kThreads) void recompute_kernel(const void* __restr
     }
 }
 
-// Loads the z of access i1 for the sign test of kBwdFromXZ (nothing otherwise).
-template <int DT, int VEC, int HINT, int BM>
-__device__ __forceinline__ void load_sign(const void* __restrict__ zs, uint64_t i1,
-                                          float (&v)[VEC]) {
+// One batch of the backward's tensors at accesses idx(0..U-1), raw: u, the
+// stored z for kBwdFromXZ, dz.
+template <int DT, int VEC, int HINT, int U, int BM, typename Index>
+__device__ __forceinline__ void load_bwd_raw(const void* __restrict__ u,
+                                             const void* __restrict__ zs,
+                                             const void* __restrict__ dz, Index idx,
+                                             raw_t<DT, VEC> (&ru)[U], raw_t<DT, VEC> (&rz)[U],
+                                             raw_t<DT, VEC> (&rg)[U]) {
+#pragma unroll
+    for (int q = 0; q < U; ++q) {
+        const uint64_t i1 = idx(q);
+        ru[q] = load_raw<DT, VEC, HINT>(u, i1);
+        if constexpr (BM == kBwdFromXZ) rz[q] = load_raw<DT, VEC, HINT>(zs, i1);
+        rg[q] = load_raw<DT, VEC, HINT>(dz, i1);
+    }
+}
+
+// The same widened to fp32 (z as zeros unless kBwdFromXZ).
+template <int DT, int VEC, int U, int BM>
+__device__ __forceinline__ void widen_bwd(const raw_t<DT, VEC> (&ru)[U],
+                                          const raw_t<DT, VEC> (&rz)[U],
+                                          const raw_t<DT, VEC> (&rg)[U], float (&tu)[U][VEC],
+                                          float (&tz)[U][VEC], float (&tg)[U][VEC]) {
+    widen<DT, VEC, U>(ru, tu);
+    widen<DT, VEC, U>(rg, tg);
     if constexpr (BM == kBwdFromXZ) {
-        load_vec<DT, VEC, HINT>(zs, i1, v);
+        widen<DT, VEC, U>(rz, tz);
     } else {
 #pragma unroll
-        for (int k = 0; k < VEC; ++k) v[k] = 0.f;
+        for (int q = 0; q < U; ++q)
+#pragma unroll
+            for (int k = 0; k < VEC; ++k) tz[q][k] = 0.f;
     }
 }
 
@@ -261,14 +329,12 @@ __global__ __launch_bounds__(kThreads) void bwd_reduce_kernel(const void* __rest
     double acc_dy = 0.0, acc_dyw = 0.0;
     uint32_t v = s.lo + threadIdx.x;
     for (; v + (U - 1) * kThreads < s.hi; v += U * kThreads) {
+        raw_t<DT, VEC> ru[U], rz[U], rg[U];
+        load_bwd_raw<DT, VEC, kHintReduceLoad, U, BM>(
+            u, zs, dz, [&](int q) { return access_index(g, cbase, v + q * kThreads); }, ru, rz, rg);
+        sched_fence();
         float tu[U][VEC], tz[U][VEC], tg[U][VEC];
-#pragma unroll
-        for (int q = 0; q < U; ++q) {
-            const uint64_t i1 = access_index(g, cbase, v + q * kThreads);
-            load_vec<DT, VEC, kHintReduceLoad>(u, i1, tu[q]);
-            load_sign<DT, VEC, kHintReduceLoad, BM>(zs, i1, tz[q]);
-            load_vec<DT, VEC, kHintReduceLoad>(dz, i1, tg[q]);
-        }
+        widen_bwd<DT, VEC, U, BM>(ru, rz, rg, tu, tz, tg);
         float sdy = 0.f, sdyw = 0.f;
 #pragma unroll
         for (int q = 0; q < U; ++q) {
@@ -283,19 +349,25 @@ __global__ __launch_bounds__(kThreads) void bwd_reduce_kernel(const void* __rest
         acc_dy += sdy;
         acc_dyw += sdyw;
     }
-    for (; v < s.hi; v += kThreads) {
-        float tu[VEC], tz[VEC], tg[VEC];
-        const uint64_t i1 = access_index(g, cbase, v);
-        load_vec<DT, VEC, kHintReduceLoad>(u, i1, tu);
-        load_sign<DT, VEC, kHintReduceLoad, BM>(zs, i1, tz);
-        load_vec<DT, VEC, kHintReduceLoad>(dz, i1, tg);
+    if (v < s.hi) {
+        raw_t<DT, VEC> ru[U], rz[U], rg[U];
+        load_bwd_raw<DT, VEC, kHintReduceLoad, U, BM>(
+            u, zs, dz, [&](int q) { return rest_index(g, cbase, s, v + q * kThreads); }, ru, rz, rg);
+        sched_fence();
+        float tu[U][VEC], tz[U][VEC], tg[U][VEC];
+        widen_bwd<DT, VEC, U, BM>(ru, rz, rg, tu, tz, tg);
         float sdy = 0.f, sdyw = 0.f;
 #pragma unroll
-        for (int k = 0; k < VEC; ++k) {
-            float dy, w;
-            el(tu[k], tz[k], tg[k], dy, w);
-            sdy += dy;
-            sdyw = fmaf(dy, w, sdyw);
+        for (int q = 0; q < U; ++q) {
+            if (v + q * kThreads < s.hi) {
+#pragma unroll
+                for (int k = 0; k < VEC; ++k) {
+                    float dy, w;
+                    el(tu[q][k], tz[q][k], tg[q][k], dy, w);
+                    sdy += dy;
+                    sdyw = fmaf(dy, w, sdyw);
+                }
+            }
         }
         acc_dy += sdy;
         acc_dyw += sdyw;
@@ -324,17 +396,14 @@ __global__ __launch_bounds__(kThreads) void bwd_apply_kernel(const void* __restr
     const uint64_t cbase = static_cast<uint64_t>(s.c) * g.vrow;
 
     uint32_t v = s.lo + threadIdx.x;
-    float tu[U][VEC], tz[U][VEC], tg[U][VEC];
+    raw_t<DT, VEC> ru[U], rz[U], rg[U];
     uint64_t idx[U];
     bool full = v + (U - 1) * kThreads < s.hi;
     if (full) {
 #pragma unroll
-        for (int q = 0; q < U; ++q) {
-            idx[q] = access_index(g, cbase, v + q * kThreads);
-            load_vec<DT, VEC, kHintBwdApplyLoad>(u, idx[q], tu[q]);
-            load_sign<DT, VEC, kHintBwdApplyLoad, BM>(zs, idx[q], tz[q]);
-            load_vec<DT, VEC, kHintBwdApplyLoad>(dzdx, idx[q], tg[q]);
-        }
+        for (int q = 0; q < U; ++q) idx[q] = access_index(g, cbase, v + q * kThreads);
+        load_bwd_raw<DT, VEC, kHintBwdApplyLoad, U, BM>(
+            u, zs, dzdx, [&](int q) { return idx[q]; }, ru, rz, rg);
     }
 
     double dbeta, dgamma;
@@ -351,6 +420,8 @@ __global__ __launch_bounds__(kThreads) void bwd_apply_kernel(const void* __restr
     }
 
     while (full) {
+        float tu[U][VEC], tz[U][VEC], tg[U][VEC];
+        widen_bwd<DT, VEC, U, BM>(ru, rz, rg, tu, tz, tg);
 #pragma unroll
         for (int q = 0; q < U; ++q) {
 #pragma unroll
@@ -361,23 +432,27 @@ __global__ __launch_bounds__(kThreads) void bwd_apply_kernel(const void* __restr
         full = v + (U - 1) * kThreads < s.hi;
         if (full) {
 #pragma unroll
-            for (int q = 0; q < U; ++q) {
-                idx[q] = access_index(g, cbase, v + q * kThreads);
-                load_vec<DT, VEC, kHintBwdApplyLoad>(u, idx[q], tu[q]);
-                load_sign<DT, VEC, kHintBwdApplyLoad, BM>(zs, idx[q], tz[q]);
-                load_vec<DT, VEC, kHintBwdApplyLoad>(dzdx, idx[q], tg[q]);
-            }
+            for (int q = 0; q < U; ++q) idx[q] = access_index(g, cbase, v + q * kThreads);
+            load_bwd_raw<DT, VEC, kHintBwdApplyLoad, U, BM>(
+                u, zs, dzdx, [&](int q) { return idx[q]; }, ru, rz, rg);
+            sched_fence();
         }
     }
-    for (; v < s.hi; v += kThreads) {
-        float ru[VEC], rz[VEC], rg[VEC];
-        const uint64_t i1 = access_index(g, cbase, v);
-        load_vec<DT, VEC, kHintBwdApplyLoad>(u, i1, ru);
-        load_sign<DT, VEC, kHintBwdApplyLoad, BM>(zs, i1, rz);
-        load_vec<DT, VEC, kHintBwdApplyLoad>(dzdx, i1, rg);
+    if (v < s.hi) {
+        load_bwd_raw<DT, VEC, kHintBwdApplyLoad, U, BM>(
+            u, zs, dzdx, [&](int q) { return rest_index(g, cbase, s, v + q * kThreads); }, ru, rz,
+            rg);
+        sched_fence();
+        float tu[U][VEC], tz[U][VEC], tg[U][VEC];
+        widen_bwd<DT, VEC, U, BM>(ru, rz, rg, tu, tz, tg);
 #pragma unroll
-        for (int k = 0; k < VEC; ++k) rg[k] = dx_of(ru[k], rz[k], rg[k]);
-        store_vec<DT, VEC, kHintBwdApplyStore>(dzdx, i1, rg);
+        for (int q = 0; q < U; ++q) {
+            if (v + q * kThreads < s.hi) {
+#pragma unroll
+                for (int k = 0; k < VEC; ++k) tg[q][k] = dx_of(tu[q][k], tz[q][k], tg[q][k]);
+                store_vec<DT, VEC, kHintBwdApplyStore>(dzdx, access_index(g, cbase, v + q * kThreads), tg[q]);
+            }
+        }
     }
 }
 
