@@ -109,18 +109,27 @@ def kernel_source_digest() -> str:
     return h.hexdigest()
 
 
-TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "backbone_r101_os8_n8_f16_hbm_traffic.md")
+def _profile(name):
+    return os.path.join(ROOT, "profiles", name)
+
+
+# The committed counter summaries, by workload index.
+TRAFFIC_SUMMARIES = {2: _profile("resnet_32x256x56x56_f32_hbm_traffic.md"),
+                     3: _profile("segcrop_4x256x192x192_f16_hbm_traffic.md"),
+                     4: _profile("wide_16x2048x28x28_bf16_hbm_traffic.md"),
+                     5: _profile("backbone_r101_os8_n8_f16_hbm_traffic.md")}
 
 
 def measured_traffic(entry_point, config):
     """HBM bytes per launch of an entry point's kernel, from the committed
-    rocprofv3 counter summary (FETCH_SIZE + WRITE_SIZE, scaled by a plain copy
-    of known size), or None when that summary does not cover this workload or
-    was taken from other kernel sources."""
-    if config != 5 or not os.path.exists(TRAFFIC_SUMMARY):
+    rocprofv3 counter summary of the workload (FETCH_SIZE + WRITE_SIZE,
+    scaled by a plain copy of known size), or None when no summary covers
+    this workload or it was taken from other kernel sources."""
+    path = TRAFFIC_SUMMARIES.get(config)
+    if path is None or not os.path.exists(path):
         return None
     fields = {}
-    for line in open(TRAFFIC_SUMMARY):
+    for line in open(path):
         if line.startswith("- ") and ": " in line:
             key, val = line[2:].split(": ", 1)
             fields[key.strip()] = val.strip().strip("`")

@@ -32,19 +32,26 @@ def _summary(tmp_path, digest, bwd=207427397, fwd=138284931):
 
 
 def test_traffic_reported_for_matching_sources(tmp_path, monkeypatch):
-    monkeypatch.setattr(bench, "TRAFFIC_SUMMARY", _summary(tmp_path, bench.kernel_source_digest()))
+    monkeypatch.setattr(bench, "TRAFFIC_SUMMARIES", {5: _summary(tmp_path, bench.kernel_source_digest())})
     assert bench.measured_traffic("iabn_backward", 5) == 207427397
     assert bench.measured_traffic("iabn_forward_train", 5) == 138284931
     assert bench.measured_traffic("iabn_forward_eval", 5) is None
-    # Only the workload the counters were taken on.
+    # Only the workloads the counters were taken on.
     assert bench.measured_traffic("iabn_backward", 2) is None
+    assert bench.measured_traffic("iabn_backward", 0) is None
 
 
 def test_traffic_withheld_for_other_sources(tmp_path, monkeypatch):
-    monkeypatch.setattr(bench, "TRAFFIC_SUMMARY", _summary(tmp_path, "0" * 64))
+    monkeypatch.setattr(bench, "TRAFFIC_SUMMARIES", {5: _summary(tmp_path, "0" * 64)})
     assert bench.measured_traffic("iabn_backward", 5) is None
-    monkeypatch.setattr(bench, "TRAFFIC_SUMMARY", str(tmp_path / "missing.md"))
+    monkeypatch.setattr(bench, "TRAFFIC_SUMMARIES", {5: str(tmp_path / "missing.md")})
     assert bench.measured_traffic("iabn_backward", 5) is None
+
+
+def test_traffic_summaries_cover_the_single_gpu_workloads():
+    for c in (2, 3, 4, 5):
+        assert c in bench.TRAFFIC_SUMMARIES
+        assert bench.TRAFFIC_SUMMARIES[c].endswith("_hbm_traffic.md")
 
 
 def test_source_digest_covers_kernels_and_header():
