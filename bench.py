@@ -88,7 +88,7 @@ def parse():
     ap.add_argument("--no-probes", action="store_true",
                     help="skip the bandwidth-ceiling probes and the activation-memory measurement")
     ap.add_argument("--phase-kernels", action="store_true",
-                    help="also time the phase entry points (the streaming kernels), one by one")
+                    help="also time the phase entry points (the streaming kernels), pass by pass")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only copy MIB MiB device to device three times and exit (a kernel of "
                          "known traffic, to scale hardware byte counters)")
@@ -139,29 +139,87 @@ def measured_traffic(entry_point, config):
     return int(val) if val else None
 
 
+class TimingEvent:
+    """A HIP event for timing only, created with hipEventDisableSystemFence.
+    A default event's record ends with a system-scope fence that writes back
+    and invalidates the GPU's caches, so the kernel after it starts cold and
+    an apply pass placed after one no longer re-reads what its reduction
+    pass left in the caches; this one records the same timestamps without
+    that fence.  Same use as torch.cuda.Event(enable_timing=True): record on
+    a torch stream, elapsed_time in ms after a synchronisation.  The HIP
+    runtime is the one torch loaded (one runtime per process)."""
+
+    DISABLE_SYSTEM_FENCE = 0x20000000
+    _rt = None
+
+    @classmethod
+    def runtime(cls):
+        if cls._rt is None:
+            import torch
+            path = os.path.join(os.path.dirname(torch.__file__), "lib", "libamdhip64.so")
+            rt = ctypes.CDLL(path if os.path.exists(path) else "libamdhip64.so.7")
+            vp = ctypes.c_void_p
+            rt.hipEventCreateWithFlags.argtypes = [ctypes.POINTER(vp), ctypes.c_uint]
+            rt.hipEventRecord.argtypes = [vp, vp]
+            rt.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), vp, vp]
+            rt.hipEventDestroy.argtypes = [vp]
+            for f in (rt.hipEventCreateWithFlags, rt.hipEventRecord, rt.hipEventElapsedTime,
+                      rt.hipEventDestroy):
+                f.restype = ctypes.c_int
+            cls._rt = rt
+        return cls._rt
+
+    def __init__(self):
+        self._h = ctypes.c_void_p()
+        rc = self.runtime().hipEventCreateWithFlags(ctypes.byref(self._h), self.DISABLE_SYSTEM_FENCE)
+        if rc != 0:
+            raise RuntimeError("hipEventCreateWithFlags failed (%d)" % rc)
+
+    def record(self, stream):
+        rc = self.runtime().hipEventRecord(self._h, ctypes.c_void_p(stream.cuda_stream))
+        if rc != 0:
+            raise RuntimeError("hipEventRecord failed (%d)" % rc)
+
+    def elapsed_time(self, end):
+        ms = ctypes.c_float()
+        rc = self.runtime().hipEventElapsedTime(ctypes.byref(ms), self._h, end._h)
+        if rc != 0:
+            raise RuntimeError("hipEventElapsedTime failed (%d)" % rc)
+        return ms.value
+
+    def __del__(self):
+        if self._h and self._rt is not None:
+            self._rt.hipEventDestroy(self._h)
+
+
 def time_phases(lib, layers, refresh, check, stream, steps, b):
-    """The phase entry points (the streaming kernels) one by one, with events."""
+    """The four phase entry points (the streaming kernels) in a step's order
+    (forward: statistics then apply per layer; backward in reverse: reduce
+    then apply), with one timing event between consecutive calls: each
+    call's time is the interval between the events around it.  Each step
+    starts from the pristine inputs (refreshed before its first event, which
+    also queues work ahead of the host); one untimed step first."""
+    calls = ([(name, fn, L, attr, bpe) for L in layers
+              for name, fn, attr, bpe in (("iabn_forward_stats", lib.iabn_forward_stats, "stats", 1),
+                                          ("iabn_forward_apply", lib.iabn_forward_apply, "fwd", 2))] +
+             [(name, fn, L, attr, bpe) for L in reversed(layers)
+              for name, fn, attr, bpe in (("iabn_backward_reduce", lib.iabn_backward_reduce, "reduce", 2),
+                                          ("iabn_backward_apply", lib.iabn_backward_apply, "bwd", 3))])
     import torch
     tot_ms, tot_bytes, launches = {}, {}, {}
-    refresh()
-    torch.cuda.synchronize()
-    calls = ([x for L in layers for x in (("iabn_forward_stats", lib.iabn_forward_stats, L.stats, 1, L.E),
-                                          ("iabn_forward_apply", lib.iabn_forward_apply, L.fwd, 2, L.E))] +
-             [x for L in reversed(layers) for x in (("iabn_backward_reduce", lib.iabn_backward_reduce, L.reduce, 2, L.E),
-                                                    ("iabn_backward_apply", lib.iabn_backward_apply, L.bwd, 3, L.E))])
-    for _ in range(steps):
-        evs = []
-        for name, fn, cargs, bpe, E in calls:
-            e0 = torch.cuda.Event(enable_timing=True)
-            e1 = torch.cuda.Event(enable_timing=True)
-            e0.record(stream)
-            check(fn(*cargs), name)
-            e1.record(stream)
-            evs.append((name, e0, e1, bpe * E * b))
+    ev = [TimingEvent() for _ in range(len(calls) + 1)]
+    for step in range(steps + 1):
+        refresh()
+        ev[0].record(stream)
+        for i, (name, fn, L, attr, _) in enumerate(calls):
+            check(fn(*getattr(L, attr)), name)
+            ev[i + 1].record(stream)
         torch.cuda.synchronize()
-        for name, e0, e1, nbytes in evs:
-            tot_ms[name] = tot_ms.get(name, 0.0) + e0.elapsed_time(e1)
-            tot_bytes[name] = tot_bytes.get(name, 0) + nbytes
+        if step == 0:
+            continue
+        for i, (name, _, L, _, bpe) in enumerate(calls):
+            tot_ms[name] = tot_ms.get(name, 0.0) + ev[i].elapsed_time(ev[i + 1])
+            tot_bytes[name] = tot_bytes.get(name, 0) + bpe * L.E * b
             launches[name] = launches.get(name, 0) + 1
     return {name: {"avg_us": round(tot_ms[name] / launches[name] * 1e3, 3),
                    "launches": launches[name],
@@ -210,8 +268,8 @@ def time_probes(layers, stream, reps, b):
                     if rc != 0:
                         raise RuntimeError("iabn_probe_launch(%s) failed: %d" % (name, rc))
             one_pass()
-            e0 = torch.cuda.Event(enable_timing=True)
-            e1 = torch.cuda.Event(enable_timing=True)
+            e0 = TimingEvent()
+            e1 = TimingEvent()
             e0.record(stream)
             for _ in range(reps):
                 one_pass()
@@ -356,7 +414,7 @@ def time_arms(lib, layers, refresh, check, stream, args, E_total, b, iabn_kernel
         torch.cuda.synchronize()
         refresh()
         torch.cuda.synchronize()
-        marks = [torch.cuda.Event(enable_timing=True) for _ in range(2 * args.steps + 1)]
+        marks = [TimingEvent() for _ in range(2 * args.steps + 1)]
         t0 = time.perf_counter()
         for i in range(args.steps):
             marks[2 * i].record(stream)
@@ -513,7 +571,7 @@ def measure(lib, args):
     torch.cuda.synchronize()
     refresh()
     torch.cuda.synchronize()
-    marks = [torch.cuda.Event(enable_timing=True) for _ in range(2 * args.steps + 1)]
+    marks = [TimingEvent() for _ in range(2 * args.steps + 1)]
     t0 = time.perf_counter()
     for i in range(args.steps):
         marks[2 * i].record(stream)
@@ -561,8 +619,8 @@ def measure(lib, args):
     # the runtime's copy kernel), chained over the same buffers: the same
     # read-write mix and working set as the passes, with no arithmetic.
     torch.cuda.synchronize()
-    c0 = torch.cuda.Event(enable_timing=True)
-    c1 = torch.cuda.Event(enable_timing=True)
+    c0 = TimingEvent()
+    c1 = TimingEvent()
     reps = max(1, args.steps // 2)
     c0.record(stream)
     for _ in range(reps):
@@ -599,7 +657,7 @@ def measure(lib, args):
     # layers: one read and one write per element.
     refresh()
     torch.cuda.synchronize()
-    ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    ev = [TimingEvent() for _ in range(args.steps + 1)]
     for L in layers:
         check(lib.iabn_forward_eval(*L.eval), "iabn_forward_eval")
     ev[0].record(stream)

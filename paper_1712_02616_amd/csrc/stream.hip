@@ -491,22 +491,49 @@ constexpr int unroll() {
     return bytes >= 16 ? 2 : (32 / bytes < 8 ? 8 : 32 / bytes);
 }
 
-// The statistics pass over slices of at least 32 16-byte accesses per thread
-// keeps 8 loads in flight instead of 2 (read-only, so nothing else holds
-// registers): 15% faster on slices of 64K fp16 values, while shorter slices,
-// whose threads would leave most of a batch of 8 to the one-by-one remainder
-// loop, keep 2.
-constexpr uint32_t kLongSliceAccesses = 32 * kThreads;
+// Long slices: on the 16-byte path, a pass whose blocks own slices of at
+// least the pass's threshold (in accesses) keeps kLongU accesses per tensor
+// in flight per thread instead of unroll()'s 2.  Few-channel layers cut into
+// many slices run 512 blocks, 2 waves per SIMD, and then need the deeper
+// batches to keep enough bytes in flight; measured on (8, 64, 256x256) and
+// (32, 64, 112x112) fp16 and (16, 32, 112x112) fp32: statistics up to 13%,
+// training apply 7-12%, backward apply up to 3% faster from 8 accesses per
+// thread up (the last, partial batch is loaded whole, so short slices lose
+// nothing to a remainder loop); the backward's reduction, which reads two
+// tensors, gains only from 32 up (6% on 32, 1-6% slower on 12 and 24).  The
+// inference apply keeps 2: 8 made it 5% slower over the backbone sweep's
+// layers and no faster on the few-channel ones.
+constexpr int kLongU = 8;
+constexpr uint32_t kLongStatsAccesses = 8 * kThreads;
+constexpr uint32_t kLongApplyAccesses = 8 * kThreads;
+constexpr uint32_t kLongReduceAccesses = 32 * kThreads;
+constexpr uint32_t kLongBwdApplyAccesses = 8 * kThreads;
+
+template <int DT, int VEC>
+constexpr bool wide_access() {
+    return VEC * sizeof(typename Elem<DT>::T) == 16;
+}
+
+// Whether a pass with threshold `min_accesses` takes the long batches.
+template <int DT, int VEC>
+bool long_slices(const Geom& g, uint32_t min_accesses) {
+    return wide_access<DT, VEC>() && g.lv >= min_accesses;
+}
+
+// The long batch where the access width has one (16-byte accesses), else
+// the default; both branches of a launch name a kernel that exists.
+template <int DT, int VEC>
+constexpr int long_unroll() {
+    return wide_access<DT, VEC>() ? kLongU : unroll<DT, VEC>();
+}
 
 template <int DT, int VEC>
 struct LaunchFwdStats {
     static void run(const void* x, const Geom& g, Partial* part, hipStream_t st) {
-        constexpr int U = unroll<DT, VEC>();
-        constexpr bool wide = VEC * sizeof(typename Elem<DT>::T) == 16;
-        if (wide && g.lv >= kLongSliceAccesses)
-            fwd_stats_kernel<DT, VEC, wide ? 4 * U : U><<<grid_of(g), kThreads, 0, st>>>(x, g, part);
+        if (long_slices<DT, VEC>(g, kLongStatsAccesses))
+            fwd_stats_kernel<DT, VEC, long_unroll<DT, VEC>()><<<grid_of(g), kThreads, 0, st>>>(x, g, part);
         else
-            fwd_stats_kernel<DT, VEC, U><<<grid_of(g), kThreads, 0, st>>>(x, g, part);
+            fwd_stats_kernel<DT, VEC, unroll<DT, VEC>()><<<grid_of(g), kThreads, 0, st>>>(x, g, part);
     }
 };
 
@@ -515,7 +542,14 @@ template <int DT, int VEC>
 struct LaunchFwdApply {
     static void run(void* xz, const Geom& g, const Partial* part, const FwdParams& prm, bool train,
                     int fm, hipStream_t st) {
-        constexpr int U = unroll<DT, VEC>();
+        if (train && long_slices<DT, VEC>(g, kLongApplyAccesses))
+            go<long_unroll<DT, VEC>()>(xz, g, part, prm, train, fm, st);
+        else
+            go<unroll<DT, VEC>()>(xz, g, part, prm, train, fm, st);
+    }
+    template <int U>
+    static void go(void* xz, const Geom& g, const Partial* part, const FwdParams& prm, bool train,
+                   int fm, hipStream_t st) {
         const dim3 grid = grid_of(g);
         if (!train)
             fwd_apply_kernel<DT, VEC, U, false, kFwdInPlace><<<grid, kThreads, 0, st>>>(xz, g, part, prm);
@@ -532,7 +566,14 @@ template <int DT, int VEC>
 struct LaunchBwdReduce {
     static void run(const void* u, const void* zs, const void* dz, const Geom& g,
                     const BwdParams& prm, int bm, Partial* part, hipStream_t st) {
-        constexpr int U = unroll<DT, VEC>();
+        if (long_slices<DT, VEC>(g, kLongReduceAccesses))
+            go<long_unroll<DT, VEC>()>(u, zs, dz, g, prm, bm, part, st);
+        else
+            go<unroll<DT, VEC>()>(u, zs, dz, g, prm, bm, part, st);
+    }
+    template <int U>
+    static void go(const void* u, const void* zs, const void* dz, const Geom& g,
+                   const BwdParams& prm, int bm, Partial* part, hipStream_t st) {
         const dim3 grid = grid_of(g);
         if (bm == kBwdFromXZ)
             bwd_reduce_kernel<DT, VEC, U, kBwdFromXZ><<<grid, kThreads, 0, st>>>(u, zs, dz, g, prm, part);
@@ -547,7 +588,14 @@ template <int DT, int VEC>
 struct LaunchBwdApply {
     static void run(const void* u, const void* zs, void* dzdx, const Geom& g, const Partial* part,
                     const BwdParams& prm, int bm, hipStream_t st) {
-        constexpr int U = unroll<DT, VEC>();
+        if (long_slices<DT, VEC>(g, kLongBwdApplyAccesses))
+            go<long_unroll<DT, VEC>()>(u, zs, dzdx, g, part, prm, bm, st);
+        else
+            go<unroll<DT, VEC>()>(u, zs, dzdx, g, part, prm, bm, st);
+    }
+    template <int U>
+    static void go(const void* u, const void* zs, void* dzdx, const Geom& g, const Partial* part,
+                   const BwdParams& prm, int bm, hipStream_t st) {
         const dim3 grid = grid_of(g);
         if (bm == kBwdFromXZ)
             bwd_apply_kernel<DT, VEC, U, kBwdFromXZ><<<grid, kThreads, 0, st>>>(u, zs, dzdx, g, part, prm);

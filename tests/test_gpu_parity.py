@@ -82,6 +82,11 @@ EDGE_CASES = [
     # Slices of 64K fp16 values on the streaming path (fewer than 256
     # channels): the statistics pass with its deeper batches of loads.
     Case("long_slices_f16", 8, 64, 65536, "f16", 42, dz_std=0.1),
+    # Long slices with ragged ends: 8.55 accesses per thread, the last slice
+    # 8.48 (one batch of 8, then a partial one), and 32.05 per thread, the
+    # last slice 31.83 (the backward's reduction takes batches of 8 as well).
+    Case("long_ragged_f16", 4, 16, 140000, "f16", 52, dz_std=0.1, gamma_sign=True),
+    Case("long_ragged_reduce_bf16", 2, 8, 2100000, "bf16", 53, dz_std=0.1),
     Case("all_negative_f16", 2, 8, 512, "f16", 21, beta_shift=-12.0),
     Case("all_positive_bf16", 2, 8, 512, "bf16", 22, beta_shift=12.0),
     Case("slope1_plain_bn_f32", 4, 8, 256, "f32", 23, slope=1.0),
