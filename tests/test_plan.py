@@ -122,6 +122,14 @@ def test_always_streaming_entry_points():
         streaming(plan(op, F16, 32, 2048, 7 * 7), access=2, xcd=1)
         # Inference accepts a single value per channel (4-byte rows: XCD order).
         streaming(plan(op, F32, 1, 4, 1), access=4, xcd=1)
+    # Below 256 channels the inference forward cuts channels into slices for
+    # about 8192 blocks (slices of at least 4096 values); the recomputation
+    # and the training passes keep about 512.
+    streaming(plan("forward_eval", F16, 8, 64, 256 * 256), blocks=8192)
+    streaming(plan("forward_eval", F16, 8, 128, 128 * 128), blocks=4096)
+    streaming(plan("forward_eval", F16, 8, 256, 128 * 128), blocks=512)
+    streaming(plan("ckpt_recompute", F16, 8, 64, 256 * 256), blocks=512)
+    streaming(plan("forward_train", F16, 8, 64, 256 * 256), blocks=512)
 
 
 def test_access_width_and_xcd_order():
