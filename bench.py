@@ -221,11 +221,14 @@ def time_phases(lib, layers, refresh, check, stream, steps, b):
             tot_ms[name] = tot_ms.get(name, 0.0) + ev[i].elapsed_time(ev[i + 1])
             tot_bytes[name] = tot_bytes.get(name, 0) + bpe * L.E * b
             launches[name] = launches.get(name, 0) + 1
-    return {name: {"avg_us": round(tot_ms[name] / launches[name] * 1e3, 3),
-                   "launches": launches[name],
-                   "alg_bytes_per_launch": tot_bytes[name] // launches[name],
-                   "achieved_gbps": round(tot_bytes[name] / (tot_ms[name] * 1e-3) / 1e9, 1)}
-            for name in tot_ms}
+    out = {name: {"avg_us": round(tot_ms[name] / launches[name] * 1e3, 3),
+                  "launches": launches[name],
+                  "alg_bytes_per_launch": tot_bytes[name] // launches[name],
+                  "achieved_gbps": round(tot_bytes[name] / (tot_ms[name] * 1e-3) / 1e9, 1)}
+           for name in tot_ms}
+    out["note"] = ("each interval holds one call and one event marker; the kernels' own "
+                   "durations are rocprofv3's")
+    return out
 
 
 # Bandwidth probes (bench_probe.hip): mix code, tensors read, tensors written
