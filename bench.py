@@ -20,7 +20,8 @@ Output: one JSON line (see the keys below).  ``value`` is elements/s of the
 whole fwd+bwd step (elements = sum over layers of N*C*H*W).  ``kernels``
 gives each entry point's average launch duration, from HIP events recorded
 on the stream inside the timed steps (at each step's start, between its
-forward and backward passes, and at its end), with its algorithmic bytes
+forward and backward passes, and at its end; timing-only events, see
+``TimingEvent``), with its algorithmic bytes
 (forward: read x, write z; backward: read z and dz, write dx).
 ``roofline`` covers the one with the larger share of the step; its
 ``traffic`` is the HBM bytes per launch that rocprofv3's FETCH_SIZE and
