@@ -71,6 +71,18 @@ inline size_t fused_lds(int blocks_per_cu) {
     return kLdsPerCU / blocks_per_cu - 2048;  // leaves room for the kernels' own reduction buffers
 }
 
+// A launch's dynamic LDS is at most 64 KB (the runtime rejects a larger
+// request and aborts the queue), so a cap takes at least 3 blocks per CU;
+// and the 1024-thread kernels, whose static LDS holds up to 144 KB of
+// accesses, leave no room for a cap's reservation at all.
+constexpr bool cap_ok(int blocks_per_cu) {
+    return blocks_per_cu == 0 || kLdsPerCU / blocks_per_cu - 2048 <= 65536;
+}
+static_assert(cap_ok(kFusedFwdBlocksPerCU) && cap_ok(kFusedBwdBlocksPerCU),
+              "a residency cap needs more than 64 KB of dynamic LDS per block");
+static_assert(kFusedFwdBlocksPerCU == 0 && kFusedBwdBlocksPerCU == 0,
+              "a residency cap does not fit beside the LDS residency of the 1024-thread kernels");
+
 // Candidate (T, R) in order of preference (each one has a kernel built in
 // launch_fwd_fused / launch_bwd_fused): the first whose threads hold the
 // whole channel is used; larger channels take the last entry, which keeps
