@@ -9,6 +9,8 @@ import os
 import subprocess
 import sys
 
+import pytest
+
 import bench
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
@@ -71,3 +73,15 @@ def test_probe_library_validates_before_launching():
     assert probe.iabn_probe_launch(1, ctypes.c_void_p((1 << 20) + 8), None, 4096, 1024, 0, None,
                                    None) == 1                              # misaligned
     assert probe.iabn_probe_launch(1, a, None, 4096, 0, 0, None, None) == 1  # no blocks
+
+
+def test_timing_event_flag_matches_the_hip_header():
+    """TimingEvent's flag is the HIP runtime's hipEventDisableSystemFence (read
+    from the installed header where there is one)."""
+    import re
+    header = "/opt/rocm/include/hip/hip_runtime_api.h"
+    if not os.path.exists(header):
+        pytest.skip("no HIP header")
+    m = re.search(r"#define\s+hipEventDisableSystemFence\s+(0x[0-9a-fA-F]+)", open(header).read())
+    assert m, "hipEventDisableSystemFence not in the header"
+    assert bench.TimingEvent.DISABLE_SYSTEM_FENCE == int(m.group(1), 16)
