@@ -119,6 +119,8 @@ typedef struct {
                              channels (or slices), for rows that do not end
                              on a 128-byte line */
     int64_t blocks;       /* blocks per kernel launch */
+    int channels_per_block; /* channel-resident: channels per block (each
+                               with threads / channels_per_block threads) */
 } iabn_plan_t;
 
 /* The kernels entry point `op` (an iabn_op_t) runs for this shape and

@@ -45,7 +45,8 @@ class _Plan(ctypes.Structure):
     _fields_ = [("channel_resident", ctypes.c_int), ("access_bytes", ctypes.c_int),
                 ("threads", ctypes.c_int), ("reg_accesses", ctypes.c_int),
                 ("lds_accesses", ctypes.c_int), ("strips", ctypes.c_int),
-                ("xcd_order", ctypes.c_int), ("blocks", ctypes.c_int64)]
+                ("xcd_order", ctypes.c_int), ("blocks", ctypes.c_int64),
+                ("channels_per_block", ctypes.c_int)]
 
 _lib = None
 _lib_lock = threading.Lock()

@@ -351,11 +351,12 @@ int iabn_plan(int op, int dtype, int64_t N, int64_t C, int64_t HW, iabn_plan_t* 
         const int64_t past_per_thread = past > 0 ? (past + fp.T - 1) / fp.T : 0;
         const int64_t lds = fused_lds_accesses(fp.T, backward, op == IABN_OP_STD_BACKWARD);
         plan->channel_resident = 1;
-        plan->threads = fp.T;
+        plan->threads = fp.T * fp.cpb;
         plan->reg_accesses = fp.R;
         plan->lds_accesses = static_cast<int>(past_per_thread < lds ? past_per_thread : lds);
         plan->strips = fused_strips(g, fp, vec * eb == 16) ? 1 : 0;
-        plan->blocks = C;
+        plan->blocks = C / fp.cpb;
+        plan->channels_per_block = fp.cpb;
     } else {
         plan->threads = kThreads;
         plan->blocks = C * static_cast<int64_t>(g.P);

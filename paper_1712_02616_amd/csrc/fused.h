@@ -82,12 +82,14 @@ __device__ __forceinline__ void unpack(raw_t<DT, VEC> r, float (&v)[VEC]) {
 // barrier every wave combines all of them itself, in the same fixed order,
 // so all waves hold the same result without a second barrier.  inv_m is
 // 1/m for the block's m values (formed off the critical path).
-template <int T>
+// With CPB channels per block (CPB groups of T threads), each group's waves
+// combine only their own group's partials.
+template <int T, int CPB = 1>
 __device__ __forceinline__ void block_moments(float shift, float s1, float s2, uint32_t nacc,
                                               uint32_t vec, double inv_m, double& mean,
                                               double& var) {
     constexpr int W = T / kWave;
-    __shared__ double red[W][4];
+    __shared__ double red[CPB * W][4];
     const double kw = __shfl(shift, 0, kWave);
     const double n = static_cast<double>(nacc) * vec;
     double d1 = s1, d2 = s2;
@@ -103,13 +105,14 @@ __device__ __forceinline__ void block_moments(float shift, float s1, float s2, u
         red[wave][3] = nw;
     }
     __syncthreads();
-    const double kref = red[0][0];
+    const uint32_t w0 = CPB > 1 ? (threadIdx.x / T) * W : 0;
+    const double kref = red[w0][0];
     double t1 = 0.0, t2 = 0.0;
     if (lane_id() < W) {
-        double tn = red[lane_id()][3];
-        t1 = red[lane_id()][1];
-        t2 = red[lane_id()][2];
-        reshift(t1, t2, tn, red[lane_id()][0], kref);
+        double tn = red[w0 + lane_id()][3];
+        t1 = red[w0 + lane_id()][1];
+        t2 = red[w0 + lane_id()][2];
+        reshift(t1, t2, tn, red[w0 + lane_id()][0], kref);
     }
     t1 = wave_sum(t1);
     t2 = wave_sum(t2);

@@ -92,11 +92,11 @@ __device__ __forceinline__ void fwd_fused_apply(void* __restrict__ xz, const Geo
 // Training forward of one channel per block (statistics, running estimates,
 // z over x), same arithmetic as fwd_stats_kernel + fwd_apply_kernel in
 // stream.hip.
-template <int DT, int VEC, int T, int R, bool STRIP, int FM>
+template <int DT, int VEC, int T, int R, bool STRIP, int FM, int CPB = 1>
 __device__ __forceinline__ void fwd_fused_channel(void* __restrict__ xz, const Geom& g,
                                                   const FwdParams& prm, uint32_t c) {
     const uint64_t cbase = static_cast<uint64_t>(c) * g.vrow;
-    const uint32_t tid = threadIdx.x;
+    const uint32_t tid = CPB > 1 ? threadIdx.x % T : threadIdx.x;
     const uint32_t nstrips = STRIP ? g.vchan / T : 0;
     // The first R accesses per thread stay in registers until the apply, so
     // this is their only read: non-temporal.  Accesses past those are read
@@ -191,7 +191,7 @@ __device__ __forceinline__ void fwd_fused_channel(void* __restrict__ xz, const G
     }
 
     double mean, var;
-    block_moments<T>(shift, s1, s2, nacc, VEC, g.inv_m, mean, var);
+    block_moments<T, CPB>(shift, s1, s2, nacc, VEC, g.inv_m, mean, var);
     uint32_t tid2 = tid;
     opaque(tid2);
 #pragma unroll
@@ -241,6 +241,18 @@ __global__ __launch_bounds__(T) void fwd_fused_kernel(void* __restrict__ xz, Geo
     fwd_fused_channel<DT, VEC, T, R, STRIP, FM>(xz, g, prm, fused_channel(g, blockIdx.x));
 }
 
+// CPB adjacent channels per block, T threads each (channel
+// CPB * blockIdx.x + threadIdx.x / T): a block's rows are then CPB times as
+// long in memory, and one barrier serves CPB reductions.  Rows of whole
+// strips only (they end on a cache line, so no XCD order).
+template <int DT, int VEC, int T, int R, bool STRIP, int FM, int CPB>
+__global__ __launch_bounds__(T * CPB) void fwd_fused_multi_kernel(void* __restrict__ xz, Geom g,
+                                                                  FwdParams prm) {
+    // T is a multiple of the wave size, so the channel is uniform per wave.
+    const uint32_t c = __builtin_amdgcn_readfirstlane(CPB * blockIdx.x + threadIdx.x / T);
+    fwd_fused_channel<DT, VEC, T, R, STRIP, FM, CPB>(xz, g, prm, c);
+}
+
 #define IABN_FUSED_CASE(TT, RR)                                                              \
     if (fp.T == TT && fp.R == RR) {                                                           \
         if (fused_strips(g, fp, true))                                                        \
@@ -261,6 +273,17 @@ template <int DT, int V, int FM>
 bool launch_v(void* xz, const Geom& g, const FusedPlan& fp, const FwdParams& prm, hipStream_t st) {
     const dim3 grid = fused_grid(g, fp);
     const size_t lds = fused_lds(kFusedFwdBlocksPerCU);
+    if (fp.cpb != 1) {
+        if constexpr (V * sizeof(typename Elem<DT>::T) == 16) {
+            if (fp.cpb == kFwdMultiChannels && fp.T == 256 && fp.R == 16 &&
+                fused_strips(g, fp, true) && g.C % kFwdMultiChannels == 0) {
+                fwd_fused_multi_kernel<DT, V, 256, 16, true, FM, kFwdMultiChannels>
+                    <<<grid, 256 * kFwdMultiChannels, lds, st>>>(xz, g, prm);
+                return true;
+            }
+        }
+        return false;
+    }
     if constexpr (V * sizeof(typename Elem<DT>::T) == 16) {
         IABN_FUSED_CASE(256, 4)
         IABN_FUSED_CASE(256, 8)

@@ -52,11 +52,22 @@ inline bool fused_few_channels_ok(int64_t C, uint32_t vchan, bool backward) {
 }
 
 struct FusedPlan {
-    int T;  // threads per block
-    int R;  // accesses per thread held in registers (per tensor)
+    int T;        // threads per channel
+    int R;        // accesses per thread held in registers (per tensor)
+    int cpb = 1;  // channels per block (T * cpb threads)
 };
 
-inline dim3 fused_grid(const Geom& g, const FusedPlan&) { return dim3(g.C); }
+inline dim3 fused_grid(const Geom& g, const FusedPlan& fp) { return dim3(g.C / fp.cpb); }
+
+// The forward's (256, 16) rung on rows of whole strips takes two adjacent
+// channels per 512-thread block (each with its own 256 threads, one block
+// barrier for both reductions) from 1024 up to 2047 channels: measured
+// (8, C, 64x64) fp16, C = 1024 25.1 -> 24.2 us and C = 1536 38.5 -> 37.0
+// (the backbone sweep's C = 1024 layers 24.8 -> 23.3), but C = 768 18.1 ->
+// 20.6 and C = 2048 50.5 -> 51.3, and four channels per block no better.
+constexpr int kFwdMultiChannels = 2;
+constexpr int64_t kFwdMultiMinChannels = 1024;
+constexpr int64_t kFwdMultiMaxChannels = 2047;
 
 // Resident blocks per CU of a fused launch (0: as many as registers allow).
 // Fewer resident blocks run the channels in several rounds, so the loads of
@@ -160,6 +171,10 @@ inline bool plan_fused(int64_t C, const Geom& g, int elem_bytes, bool backward, 
             *out = ladder[i];
             if (!backward && C >= kOneWaveMinChannels && out->T == 256 && out->R == 8)
                 *out = kOneWaveRung;
+            if (!backward && wide && C >= kFwdMultiMinChannels && C <= kFwdMultiMaxChannels &&
+                C % kFwdMultiChannels == 0 && !g.xcd_order && out->T == 256 && out->R == 16 &&
+                g.vrow % 256 == 0 && g.vchan / 256 >= 16)
+                out->cpb = kFwdMultiChannels;
             return true;
         }
     }

@@ -100,6 +100,9 @@ EDGE_CASES = [
     Case("manych_c1300_bf16", 4, 1300, 8192, "bf16", 29, dz_std=0.1),
     Case("manych_c520_f32", 4, 520, 4096, "f32", 30, dz_std=0.1),
     Case("manych_t256_c512_f16", 16, 512, 2048, "f16", 31, dz_std=0.1),
+    # Two channels per forward block (1024-2047 channels of 4096 accesses on
+    # rows of whole strips; manych_c1300_bf16 above takes them as well).
+    Case("pair_c1536_f32", 8, 1536, 2048, "f32", 54, dz_std=0.1, gamma_sign=True),
     # Channels of 1025-2048 accesses: the (256, 8) rung, strip-addressed.
     Case("rung256x8_strip_f16", 8, 300, 2048, "f16", 40, dz_std=0.1, gamma_sign=True),
     Case("rung256x8_strip_f32", 4, 264, 2048, "f32", 41),

@@ -17,9 +17,11 @@ def plan(op, dtype, N, C, HW):
     return iabn.iabn_plan(op, dtype, N, C, HW)
 
 
-def fused(p, T, R, lds=0, strips=None, access=16, xcd=0, blocks=None):
+def fused(p, T, R, lds=0, strips=None, access=16, xcd=0, blocks=None, cpb=1):
+    """T: threads per channel; cpb: channels per block."""
     assert p["channel_resident"] == 1, p
-    assert (p["threads"], p["reg_accesses"], p["lds_accesses"]) == (T, R, lds), p
+    assert p["channels_per_block"] == cpb, p
+    assert (p["threads"], p["reg_accesses"], p["lds_accesses"]) == (T * cpb, R, lds), p
     assert p["access_bytes"] == access and p["xcd_order"] == xcd, p
     if strips is not None:
         assert p["strips"] == strips, p
@@ -29,6 +31,7 @@ def fused(p, T, R, lds=0, strips=None, access=16, xcd=0, blocks=None):
 
 def streaming(p, access=16, xcd=0, blocks=None):
     assert p["channel_resident"] == 0 and p["threads"] == 256, p
+    assert p["channels_per_block"] == 0, p
     assert p["reg_accesses"] == p["lds_accesses"] == p["strips"] == 0, p
     assert p["access_bytes"] == access and p["xcd_order"] == xcd, p
     if blocks is not None:
@@ -44,7 +47,26 @@ def test_backbone_sweep_layers(op):
     fused(plan(op, F16, 8, 256, 128 * 128), 1024, 11 if bwd else 16, lds=4 if bwd else 0,
           strips=1, blocks=256)
     for C in (512, 1024, 2048):
-        fused(plan(op, F16, 8, C, 64 * 64), 256, 16, strips=1, blocks=C)
+        # The forward takes two channels per block from 1024 to 2047 channels.
+        cpb = 2 if C == 1024 and not bwd else 1
+        fused(plan(op, F16, 8, C, 64 * 64), 256, 16, strips=1, blocks=C // cpb, cpb=cpb)
+
+
+def test_two_channel_forward_blocks():
+    """The forward's (256, 16) rung on rows of whole strips: two adjacent
+    channels per block for 1024-2047 (even) channels, every forward mode;
+    one per block outside that range, for odd channel counts, for rows that
+    take the general mapping, and in the backward."""
+    for op in ("forward_train", "std_forward", "ckpt_forward"):
+        fused(plan(op, F16, 8, 1024, 64 * 64), 256, 16, strips=1, blocks=512, cpb=2)
+        fused(plan(op, F16, 8, 1536, 64 * 64), 256, 16, strips=1, blocks=768, cpb=2)
+        fused(plan(op, F16, 8, 2046, 64 * 64), 256, 16, strips=1, blocks=1023, cpb=2)
+    fused(plan("forward_train", F16, 8, 1022, 64 * 64), 256, 16, strips=1, blocks=1022)
+    fused(plan("forward_train", F16, 8, 1025, 64 * 64), 256, 16, strips=1, blocks=1025)
+    fused(plan("forward_train", F32, 8, 1024, 32 * 64), 256, 16, strips=1, blocks=512, cpb=2)
+    # Rows of 32x32 fp16 (128 accesses) hold no 256-wide strip: general mapping.
+    fused(plan("forward_train", F16, 32, 1024, 32 * 32), 256, 16, strips=0, blocks=1024)
+    fused(plan("backward", F16, 8, 1024, 64 * 64), 256, 16, strips=1, blocks=1024)
 
 
 def test_parity_workloads():
@@ -109,8 +131,8 @@ def test_comparison_blocks():
     # The standard block keeps three tensors in the backward: 3 per tensor in LDS.
     fused(plan("std_backward", F16, 8, 256, 128 * 128), 1024, 11, lds=3, strips=1)
     fused(plan("ckpt_backward", F16, 8, 256, 128 * 128), 1024, 11, lds=4, strips=1)
-    fused(plan("std_forward", F16, 8, 1024, 64 * 64), 256, 16, strips=1)
-    fused(plan("ckpt_forward", F16, 8, 1024, 64 * 64), 256, 16, strips=1)
+    fused(plan("std_forward", F16, 8, 1024, 64 * 64), 256, 16, strips=1, cpb=2)
+    fused(plan("ckpt_forward", F16, 8, 1024, 64 * 64), 256, 16, strips=1, cpb=2)
     # Narrow rows: the comparison blocks take the streaming kernels.
     streaming(plan("std_forward", F16, 32, 2048, 7 * 7), access=2, xcd=1)
     streaming(plan("ckpt_backward", F16, 32, 2048, 7 * 7), access=2, xcd=1)
@@ -186,8 +208,8 @@ def test_narrower_accesses_change_the_plan():
     standard block leaves the channel-resident kernels, InPlace-ABN's forward
     takes another rung.  (8, 1024, 4100) fp16 has such rows; the aligned
     neighbour (8, 1024, 4096) does not."""
-    fused(plan("std_forward", F16, 8, 1024, 4096), 256, 16, strips=1)
+    fused(plan("std_forward", F16, 8, 1024, 4096), 256, 16, strips=1, cpb=2)
     streaming(plan("std_forward", F16, 8, 1024, 4100), access=8, xcd=1)
     streaming(plan("std_backward", F16, 8, 1024, 4100), access=8, xcd=1)
-    fused(plan("forward_train", F16, 8, 1024, 4096), 256, 16, strips=1)
+    fused(plan("forward_train", F16, 8, 1024, 4096), 256, 16, strips=1, cpb=2)
     fused(plan("forward_train", F16, 8, 1024, 4100), 1024, 16, lds=0, access=8, xcd=1)
