@@ -120,11 +120,12 @@ __device__ __forceinline__ void block_moments(float shift, float s1, float s2, u
     var = fmax(t2 - t1 * t1 * inv_m, 0.0) * inv_m;
 }
 
-// Two sums over a block, returned in every thread (one barrier, as above).
-template <int T>
+// Two sums over a block, returned in every thread (one barrier, as above;
+// with CPB channels per block, over the thread's group of T threads).
+template <int T, int CPB = 1>
 __device__ __forceinline__ void block_sums(double a, double b, double& sa, double& sb) {
     constexpr int W = T / kWave;
-    __shared__ double red[W][2];
+    __shared__ double red[CPB * W][2];
     a = wave_sum(a);
     b = wave_sum(b);
     const uint32_t wave = threadIdx.x / kWave;
@@ -133,8 +134,9 @@ __device__ __forceinline__ void block_sums(double a, double b, double& sa, doubl
         red[wave][1] = b;
     }
     __syncthreads();
-    double t1 = lane_id() < W ? red[lane_id()][0] : 0.0;
-    double t2 = lane_id() < W ? red[lane_id()][1] : 0.0;
+    const uint32_t w0 = CPB > 1 ? (threadIdx.x / T) * W : 0;
+    double t1 = lane_id() < W ? red[w0 + lane_id()][0] : 0.0;
+    double t2 = lane_id() < W ? red[w0 + lane_id()][1] : 0.0;
     sa = wave_sum(t1);
     sb = wave_sum(t2);
 }

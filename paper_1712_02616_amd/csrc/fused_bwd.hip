@@ -16,7 +16,7 @@ namespace {
 // stream.hip.  u is z, x or xhat (see BwdSign).  kBwdFromXZ reads the stored
 // z as well but keeps only its signs (one bit per element) for the apply
 // phase.
-template <int DT, int VEC, int T, int R, bool STRIP, int BM>
+template <int DT, int VEC, int T, int R, bool STRIP, int BM, int CPB = 1>
 __device__ __forceinline__ void bwd_fused_channel(const void* __restrict__ u,
                                                   const void* __restrict__ zs,
                                                   void* __restrict__ dzdx, const Geom& g,
@@ -24,7 +24,7 @@ __device__ __forceinline__ void bwd_fused_channel(const void* __restrict__ u,
     constexpr bool XZ = BM == kBwdFromXZ;
     constexpr int NW = XZ ? (R * VEC + 31) / 32 : 1;
     const uint64_t cbase = static_cast<uint64_t>(c) * g.vrow;
-    const uint32_t tid = threadIdx.x;
+    const uint32_t tid = CPB > 1 ? threadIdx.x % T : threadIdx.x;
     const uint32_t nstrips = STRIP ? g.vchan / T : 0;
     // Register-resident accesses non-temporal, the rest cached (see
     // fwd_fused_channel).  kBwdFromXZ first loads z (into the registers x
@@ -219,7 +219,7 @@ __device__ __forceinline__ void bwd_fused_channel(const void* __restrict__ u,
     }
 
     double dbeta, sdyw;
-    block_sums<T>(acc_dy, acc_dyw, dbeta, sdyw);
+    block_sums<T, CPB>(acc_dy, acc_dyw, dbeta, sdyw);
     uint32_t tid2 = tid;
     opaque(tid2);
 #pragma unroll
@@ -314,6 +314,17 @@ __global__ __launch_bounds__(T) void bwd_fused_kernel(const void* __restrict__ u
     bwd_fused_channel<DT, VEC, T, R, STRIP, BM>(u, zs, dzdx, g, prm, fused_channel(g, blockIdx.x));
 }
 
+// CPB adjacent channels per block, T threads each (channel
+// CPB * blockIdx.x + threadIdx.x / T; see fwd_fused_multi_kernel).
+template <int DT, int VEC, int T, int R, bool STRIP, int BM, int CPB>
+__global__ __launch_bounds__(T * CPB) void bwd_fused_multi_kernel(const void* __restrict__ u,
+                                                                  const void* __restrict__ zs,
+                                                                  void* __restrict__ dzdx, Geom g,
+                                                                  BwdParams prm) {
+    const uint32_t c = __builtin_amdgcn_readfirstlane(CPB * blockIdx.x + threadIdx.x / T);
+    bwd_fused_channel<DT, VEC, T, R, STRIP, BM, CPB>(u, zs, dzdx, g, prm, c);
+}
+
 #define IABN_FUSED_CASE(TT, RR)                                                              \
     if (fp.T == TT && fp.R == RR) {                                                           \
         if (fused_strips(g, fp, true))                                                        \
@@ -334,6 +345,17 @@ bool launch_v(const void* u, const void* zs, void* dzdx, const Geom& g, const Fu
               const BwdParams& prm, hipStream_t st) {
     const dim3 grid = fused_grid(g, fp);
     const size_t lds = fused_lds(kFusedBwdBlocksPerCU);
+    if (fp.cpb != 1) {
+        if constexpr (V * sizeof(typename Elem<DT>::T) == 16 && BM == kBwdFromZ) {
+            if (fp.cpb == kBwdMultiChannels && fp.T == 256 && fp.R == 16 &&
+                fused_strips(g, fp, true) && g.C % kBwdMultiChannels == 0) {
+                bwd_fused_multi_kernel<DT, V, 256, 16, true, BM, kBwdMultiChannels>
+                    <<<grid, 256 * kBwdMultiChannels, lds, st>>>(u, zs, dzdx, g, prm);
+                return true;
+            }
+        }
+        return false;
+    }
     if constexpr (V * sizeof(typename Elem<DT>::T) == 16) {
         IABN_FUSED_CASE(256, 4)
         IABN_FUSED_CASE(256, 8)

@@ -69,6 +69,16 @@ constexpr int kFwdMultiChannels = 2;
 constexpr int64_t kFwdMultiMinChannels = 1024;
 constexpr int64_t kFwdMultiMaxChannels = 2047;
 
+// The backward's (256, 16) rung takes two adjacent channels per 512-thread
+// block (one such block per CU: 166 registers) where that makes whole rounds
+// of one block on every CU, C = 512 or 1024 on the 256 CUs: (8, C, 64x64)
+// fp16, C = 512 20.6 -> 18.1 us, C = 1024 37.6 -> 37.1 (the backbone sweep's
+// C = 1024 layers 37.6 -> 36.8); slower for C = 768 (27.8 -> 31.2), 1280
+// (44.6 -> 49.2), 1536 (53.2 -> 56.7) and 2048 (72.4 -> 81.7).
+constexpr int kBwdMultiChannels = 2;
+constexpr int64_t kCUs = 256;
+constexpr int64_t kBwdMultiMaxRounds = 2;
+
 // Resident blocks per CU of a fused launch (0: as many as registers allow).
 // Fewer resident blocks run the channels in several rounds, so the loads of
 // a later round overlap the stores of an earlier one instead of every block
@@ -175,6 +185,10 @@ inline bool plan_fused(int64_t C, const Geom& g, int elem_bytes, bool backward, 
                 C % kFwdMultiChannels == 0 && !g.xcd_order && out->T == 256 && out->R == 16 &&
                 g.vrow % 256 == 0 && g.vchan / 256 >= 16)
                 out->cpb = kFwdMultiChannels;
+            if (backward && narrow_ok && wide && C % (kBwdMultiChannels * kCUs) == 0 &&
+                C <= kBwdMultiMaxRounds * kBwdMultiChannels * kCUs && !g.xcd_order &&
+                out->T == 256 && out->R == 16 && g.vrow % 256 == 0 && g.vchan / 256 >= 16)
+                out->cpb = kBwdMultiChannels;
             return true;
         }
     }

@@ -30,14 +30,15 @@ pytestmark = [pytest.mark.gpu,
 
 _BY_ID = {c.id: c for c in ALL_CASES}
 # Streaming shapes (few channels, odd HW, ragged slices), every fused ladder
-# rung and storage type, and the numerically awkward cases.
+# rung and storage type, the two-channel blocks, and the numerically awkward
+# cases.
 ARM_CASES = [_BY_ID[k] for k in (
     "cfg1_tiny_f32", "cfg2_resnet_f32", "cfg3_segcrop_f16", "cfg4_wide_bf16", "odd_hw49_bf16",
     "hw1_f32", "n1_m2_f16", "ragged_slices_f16", "ragged_odd_f32", "all_negative_f16",
     "all_positive_bf16", "slope1_plain_bn_f32", "large_mean_f32", "eps_large_bf16",
     "manych_c600_f16", "manych_c520_f32", "manych_t256_c512_f16", "rung256x8_strip_f16",
     "rung256x8_strip_f32", "fewch_c128_f16", "fewch_c64_f32", "narrow8_hw196_f16",
-    "narrow4_hw98_bf16", "narrow4_hw49_f32")]
+    "narrow4_hw98_bf16", "narrow4_hw49_f32", "pair_c1536_f32", "pair_bwd_c512_f32")]
 CHAIN_CASES = [_BY_ID[k] for k in ("cfg1_tiny_f32", "odd_hw49_f16", "ragged_slices_bf16",
                                    "manych_c520_f32", "manych_t256_c512_f16", "cfg4_wide_bf16")]
 

@@ -47,8 +47,9 @@ def test_backbone_sweep_layers(op):
     fused(plan(op, F16, 8, 256, 128 * 128), 1024, 11 if bwd else 16, lds=4 if bwd else 0,
           strips=1, blocks=256)
     for C in (512, 1024, 2048):
-        # The forward takes two channels per block from 1024 to 2047 channels.
-        cpb = 2 if C == 1024 and not bwd else 1
+        # Two channels per block: the forward from 1024 to 2047 channels, the
+        # backward for 512 and 1024 (whole rounds of one block per CU).
+        cpb = 2 if (C in (512, 1024) if bwd else C == 1024) else 1
         fused(plan(op, F16, 8, C, 64 * 64), 256, 16, strips=1, blocks=C // cpb, cpb=cpb)
 
 
@@ -66,7 +67,22 @@ def test_two_channel_forward_blocks():
     fused(plan("forward_train", F32, 8, 1024, 32 * 64), 256, 16, strips=1, blocks=512, cpb=2)
     # Rows of 32x32 fp16 (128 accesses) hold no 256-wide strip: general mapping.
     fused(plan("forward_train", F16, 32, 1024, 32 * 32), 256, 16, strips=0, blocks=1024)
-    fused(plan("backward", F16, 8, 1024, 64 * 64), 256, 16, strips=1, blocks=1024)
+
+
+
+def test_two_channel_backward_blocks():
+    """InPlace-ABN's backward (I and II) takes two adjacent channels per
+    (256, 16) block where that fills whole rounds of one block per CU (512
+    and 1024 channels on 256 CUs); the comparison blocks' backwards do not."""
+    fused(plan("backward", F16, 8, 512, 64 * 64), 256, 16, strips=1, blocks=256, cpb=2)
+    fused(plan("backward", F16, 8, 1024, 64 * 64), 256, 16, strips=1, blocks=512, cpb=2)
+    fused(plan("backward", F32, 8, 512, 32 * 64), 256, 16, strips=1, blocks=256, cpb=2)
+    for C in (256, 768, 1536, 2048):
+        fused(plan("backward", F16, 8, C, 64 * 64), 256, 16, strips=1, blocks=C)
+    for op in ("std_backward", "ckpt_backward"):
+        fused(plan(op, F16, 8, 512, 64 * 64), 256, 16, strips=1, blocks=512)
+    # Rows that take the general mapping keep one channel per block.
+    fused(plan("backward", F16, 32, 512, 32 * 32), 256, 16, strips=0, blocks=512)
 
 
 def test_parity_workloads():
