@@ -347,11 +347,17 @@ bool launch_v(const void* u, const void* zs, void* dzdx, const Geom& g, const Fu
     const size_t lds = fused_lds(kFusedBwdBlocksPerCU);
     if (fp.cpb != 1) {
         if constexpr (V * sizeof(typename Elem<DT>::T) == 16 && BM == kBwdFromZ) {
-            if (fp.cpb == kBwdMultiChannels && fp.T == 256 && fp.R == 16 &&
-                fused_strips(g, fp, true) && g.C % kBwdMultiChannels == 0) {
-                bwd_fused_multi_kernel<DT, V, 256, 16, true, BM, kBwdMultiChannels>
-                    <<<grid, 256 * kBwdMultiChannels, lds, st>>>(u, zs, dzdx, g, prm);
-                return true;
+            if (fp.T == 256 && fp.R == 16 && fused_strips(g, fp, true) && g.C % fp.cpb == 0) {
+                if (fp.cpb == 2) {
+                    bwd_fused_multi_kernel<DT, V, 256, 16, true, BM, 2>
+                        <<<grid, 512, lds, st>>>(u, zs, dzdx, g, prm);
+                    return true;
+                }
+                if (fp.cpb == 3) {
+                    bwd_fused_multi_kernel<DT, V, 256, 16, true, BM, 3>
+                        <<<grid, 768, lds, st>>>(u, zs, dzdx, g, prm);
+                    return true;
+                }
             }
         }
         return false;

@@ -69,15 +69,21 @@ constexpr int kFwdMultiChannels = 2;
 constexpr int64_t kFwdMultiMinChannels = 1024;
 constexpr int64_t kFwdMultiMaxChannels = 2047;
 
-// The backward's (256, 16) rung takes two adjacent channels per 512-thread
-// block (one such block per CU: 166 registers) where that makes whole rounds
-// of one block on every CU, C = 512 or 1024 on the 256 CUs: (8, C, 64x64)
-// fp16, C = 512 20.6 -> 18.1 us, C = 1024 37.6 -> 37.1 (the backbone sweep's
-// C = 1024 layers 37.6 -> 36.8); slower for C = 768 (27.8 -> 31.2), 1280
-// (44.6 -> 49.2), 1536 (53.2 -> 56.7) and 2048 (72.4 -> 81.7).
-constexpr int kBwdMultiChannels = 2;
+// The backward's (256, 16) rung (166 registers: up to 3 waves per SIMD)
+// takes several adjacent channels per block where the launch is then one
+// round of one block on every CU, C = 512 (two channels per 512-thread
+// block) or 768 (three per 768-thread block) on the 256 CUs, and two per
+// block for C = 1024 (two rounds): (8, C, 64x64) fp16, C = 512 20.6 -> 18.1
+// us, C = 768 27.3 -> 25.7, C = 1024 37.6 -> 37.1 (the backbone sweep's
+// C = 1024 layers 37.6 -> 36.8).  Where it adds rounds or leaves CUs with
+// unequal shares it is slower: two per block C = 768 27.8 -> 31.2, 1280
+// 44.6 -> 49.2, 1536 53.2 -> 56.7, 2048 72.4 -> 81.7; three per block
+// C = 1536 53.7 -> 56.3.
 constexpr int64_t kCUs = 256;
-constexpr int64_t kBwdMultiMaxRounds = 2;
+
+inline int bwd_channels_per_block(int64_t C) {
+    return C == 2 * kCUs ? 2 : C == 3 * kCUs ? 3 : C == 4 * kCUs ? 2 : 1;
+}
 
 // Resident blocks per CU of a fused launch (0: as many as registers allow).
 // Fewer resident blocks run the channels in several rounds, so the loads of
@@ -185,10 +191,9 @@ inline bool plan_fused(int64_t C, const Geom& g, int elem_bytes, bool backward, 
                 C % kFwdMultiChannels == 0 && !g.xcd_order && out->T == 256 && out->R == 16 &&
                 g.vrow % 256 == 0 && g.vchan / 256 >= 16)
                 out->cpb = kFwdMultiChannels;
-            if (backward && narrow_ok && wide && C % (kBwdMultiChannels * kCUs) == 0 &&
-                C <= kBwdMultiMaxRounds * kBwdMultiChannels * kCUs && !g.xcd_order &&
-                out->T == 256 && out->R == 16 && g.vrow % 256 == 0 && g.vchan / 256 >= 16)
-                out->cpb = kBwdMultiChannels;
+            if (backward && narrow_ok && wide && !g.xcd_order && out->T == 256 && out->R == 16 &&
+                g.vrow % 256 == 0 && g.vchan / 256 >= 16)
+                out->cpb = bwd_channels_per_block(C);
             return true;
         }
     }

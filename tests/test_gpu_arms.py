@@ -38,7 +38,8 @@ ARM_CASES = [_BY_ID[k] for k in (
     "all_positive_bf16", "slope1_plain_bn_f32", "large_mean_f32", "eps_large_bf16",
     "manych_c600_f16", "manych_c520_f32", "manych_t256_c512_f16", "rung256x8_strip_f16",
     "rung256x8_strip_f32", "fewch_c128_f16", "fewch_c64_f32", "narrow8_hw196_f16",
-    "narrow4_hw98_bf16", "narrow4_hw49_f32", "pair_c1536_f32", "pair_bwd_c512_f32")]
+    "narrow4_hw98_bf16", "narrow4_hw49_f32", "pair_c1536_f32", "pair_bwd_c512_f32",
+    "triple_bwd_c768_f16")]
 CHAIN_CASES = [_BY_ID[k] for k in ("cfg1_tiny_f32", "odd_hw49_f16", "ragged_slices_bf16",
                                    "manych_c520_f32", "manych_t256_c512_f16", "cfg4_wide_bf16")]
 

@@ -103,10 +103,11 @@ EDGE_CASES = [
     # Two channels per forward block (1024-2047 channels of 4096 accesses on
     # rows of whole strips; manych_c1300_bf16 above takes them as well).
     Case("pair_c1536_f32", 8, 1536, 2048, "f32", 54, dz_std=0.1, gamma_sign=True),
-    # Two channels per backward block (512 or 1024 channels of 4096 accesses
-    # on rows of whole strips; manych_t256_c512_f16 takes them as well).
+    # Several channels per backward block (512, 768 or 1024 channels of 4096
+    # accesses on rows of whole strips; manych_t256_c512_f16 takes them too).
     Case("pair_bwd_c512_f32", 8, 512, 2048, "f32", 55, dz_std=0.1, gamma_sign=True),
     Case("pair_bwd_c1024_bf16", 4, 1024, 8192, "bf16", 56, dz_std=0.1),
+    Case("triple_bwd_c768_f16", 8, 768, 4096, "f16", 57, dz_std=0.1, gamma_sign=True),
     # Channels of 1025-2048 accesses: the (256, 8) rung, strip-addressed.
     Case("rung256x8_strip_f16", 8, 300, 2048, "f16", 40, dz_std=0.1, gamma_sign=True),
     Case("rung256x8_strip_f32", 4, 264, 2048, "f32", 41),

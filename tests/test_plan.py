@@ -70,14 +70,16 @@ def test_two_channel_forward_blocks():
 
 
 
-def test_two_channel_backward_blocks():
-    """InPlace-ABN's backward (I and II) takes two adjacent channels per
-    (256, 16) block where that fills whole rounds of one block per CU (512
-    and 1024 channels on 256 CUs); the comparison blocks' backwards do not."""
+def test_multi_channel_backward_blocks():
+    """InPlace-ABN's backward (I and II) takes several adjacent channels per
+    (256, 16) block where the launch is then one round of one block per CU
+    (512 channels: two per block, 768: three, on 256 CUs) and two per block
+    for 1024 channels; the comparison blocks' backwards take one."""
     fused(plan("backward", F16, 8, 512, 64 * 64), 256, 16, strips=1, blocks=256, cpb=2)
+    fused(plan("backward", F16, 8, 768, 64 * 64), 256, 16, strips=1, blocks=256, cpb=3)
     fused(plan("backward", F16, 8, 1024, 64 * 64), 256, 16, strips=1, blocks=512, cpb=2)
     fused(plan("backward", F32, 8, 512, 32 * 64), 256, 16, strips=1, blocks=256, cpb=2)
-    for C in (256, 768, 1536, 2048):
+    for C in (256, 1280, 1536, 2048):
         fused(plan("backward", F16, 8, C, 64 * 64), 256, 16, strips=1, blocks=C)
     for op in ("std_backward", "ckpt_backward"):
         fused(plan(op, F16, 8, 512, 64 * 64), 256, 16, strips=1, blocks=512)
