@@ -346,7 +346,7 @@ bool launch_v(const void* u, const void* zs, void* dzdx, const Geom& g, const Fu
     const dim3 grid = fused_grid(g, fp);
     const size_t lds = fused_lds(kFusedBwdBlocksPerCU);
     if (fp.cpb != 1) {
-        if constexpr (V * sizeof(typename Elem<DT>::T) == 16 && BM == kBwdFromZ) {
+        if constexpr (V * sizeof(typename Elem<DT>::T) == 16) {
             if (fp.T == 256 && fp.R == 16 && fused_strips(g, fp, true) && g.C % fp.cpb == 0) {
                 if (fp.cpb == 2) {
                     bwd_fused_multi_kernel<DT, V, 256, 16, true, BM, 2>

@@ -191,7 +191,7 @@ inline bool plan_fused(int64_t C, const Geom& g, int elem_bytes, bool backward, 
                 C % kFwdMultiChannels == 0 && !g.xcd_order && out->T == 256 && out->R == 16 &&
                 g.vrow % 256 == 0 && g.vchan / 256 >= 16)
                 out->cpb = kFwdMultiChannels;
-            if (backward && narrow_ok && wide && !g.xcd_order && out->T == 256 && out->R == 16 &&
+            if (backward && wide && !g.xcd_order && out->T == 256 && out->R == 16 &&
                 g.vrow % 256 == 0 && g.vchan / 256 >= 16)
                 out->cpb = bwd_channels_per_block(C);
             return true;

@@ -71,10 +71,10 @@ def test_two_channel_forward_blocks():
 
 
 def test_multi_channel_backward_blocks():
-    """InPlace-ABN's backward (I and II) takes several adjacent channels per
-    (256, 16) block where the launch is then one round of one block per CU
-    (512 channels: two per block, 768: three, on 256 CUs) and two per block
-    for 1024 channels; the comparison blocks' backwards take one."""
+    """Every backward (InPlace-ABN I and II, the standard block, the
+    checkpointing) takes several adjacent channels per (256, 16) block where
+    the launch is then one round of one block per CU (512 channels: two per
+    block, 768: three, on 256 CUs) and two per block for 1024 channels."""
     fused(plan("backward", F16, 8, 512, 64 * 64), 256, 16, strips=1, blocks=256, cpb=2)
     fused(plan("backward", F16, 8, 768, 64 * 64), 256, 16, strips=1, blocks=256, cpb=3)
     fused(plan("backward", F16, 8, 1024, 64 * 64), 256, 16, strips=1, blocks=512, cpb=2)
@@ -82,7 +82,9 @@ def test_multi_channel_backward_blocks():
     for C in (256, 1280, 1536, 2048):
         fused(plan("backward", F16, 8, C, 64 * 64), 256, 16, strips=1, blocks=C)
     for op in ("std_backward", "ckpt_backward"):
-        fused(plan(op, F16, 8, 512, 64 * 64), 256, 16, strips=1, blocks=512)
+        fused(plan(op, F16, 8, 512, 64 * 64), 256, 16, strips=1, blocks=256, cpb=2)
+        fused(plan(op, F16, 8, 768, 64 * 64), 256, 16, strips=1, blocks=256, cpb=3)
+        fused(plan(op, F16, 8, 2048, 64 * 64), 256, 16, strips=1, blocks=2048)
     # Rows that take the general mapping keep one channel per block.
     fused(plan("backward", F16, 32, 512, 32 * 32), 256, 16, strips=0, blocks=512)
 
