@@ -21,8 +21,9 @@ pytestmark = [pytest.mark.gpu,
               pytest.mark.skipif(not torch.cuda.is_available(), reason="needs a HIP GPU")]
 
 
-@pytest.mark.parametrize("shape,dtype", [((4, 300, 1024), "f16"), ((3, 5, 49), "f32")],
-                         ids=["fused_f16", "streaming_f32"])
+@pytest.mark.parametrize("shape,dtype", [((4, 300, 1024), "f16"), ((3, 5, 49), "f32"),
+                                         ((8, 1024, 4096), "f16")],
+                         ids=["fused_f16", "streaming_f32", "multi_channel_f16"])
 def test_graph_replay_matches_eager(shape, dtype):
     N, C, HW = shape
     inp = workloads.make_layer(N, C, HW, dtype, seed=77, dz_std=0.1, gamma_sign=True)
